@@ -1,0 +1,107 @@
+/*
+ * o1d.h - C ABI of the MI355X (gfx950) library for depthwise convolution
+ * with oriented 1D kernels.
+ *
+ * The operation is Definition 1, Eq. (1)-(2) of Kirchmeyer & Deng,
+ * "Convolutional Networks with Oriented 1D Kernels" (ICCV 2023), with the
+ * appendix "1D formulation" coordinate equation and the appendix "Padding"
+ * rule (odd K, pad = K/2 inside the floor), stride 1 and zero padding:
+ *
+ *   y[n,c,p,q] = sum_{k=0}^{K-1} x[n,c, p + dh_c(k), q + dw_c(k)] * w[c,k]
+ *   dh_c(k) = floor(-(k - K/2) * sin(theta_c)),
+ *   dw_c(k) = floor( (k - K/2) * cos(theta_c)),
+ *
+ * where an x index outside [0,H) x [0,W) reads zero.  theta_c is given in
+ * degrees; a product (k - K/2) * sin or cos that lies within 1e-9 of an
+ * integer is taken to be that integer before the floor (so 0, 90, 30 ...
+ * degrees give the exact-arithmetic offsets).  Taps that land on the same
+ * pixel are summed.
+ *
+ * Layouts (all tensors dense, row-major, no strides):
+ *   x, y, dy, dx : [N][C][H][W] in the element type `dtype`
+ *   w, dw        : [C][K]       in the element type `dtype`
+ *   theta_deg    : [C] float32 degrees, any finite value
+ * Output size equals input size (P = H, Q = W).
+ *
+ * Memory and ownership: every tensor pointer is a DEVICE pointer owned by the
+ * caller.  The library never allocates, frees or retains device memory on
+ * these calls and keeps no per-call state, so calls are re-entrant.  All work
+ * is enqueued asynchronously on `stream` (a hipStream_t; NULL selects the
+ * null stream); the call returns after the enqueue.  Output buffers must not
+ * alias input buffers.
+ *
+ * Precision: O1D_F32 computes and stores float32.  O1D_BF16 reads bfloat16,
+ * accumulates in float32 and rounds the stored results to bfloat16 with
+ * round-to-nearest-even.
+ *
+ * Errors: every argument check runs before any device work is enqueued; a
+ * non-OK status means nothing was enqueued, except O1D_ERR_HIP, which reports
+ * a failed kernel launch.  o1d_last_error() returns a human-readable detail
+ * for the calling thread's most recent non-OK status.  Device faults, if
+ * any, surface at the caller's next synchronisation.
+ *
+ * Empty tensors: a zero N, C, H or W is valid.  Nothing is launched, except
+ * that o1d_bwd_weight with C > 0 writes zeros to dw (an empty sum).
+ */
+#ifndef O1D_H_
+#define O1D_H_
+
+#include <stddef.h>
+
+#ifdef __cplusplus
+extern "C" {
+#endif
+
+typedef enum {
+  O1D_F32 = 0,  /* float32 storage and arithmetic */
+  O1D_BF16 = 1  /* bfloat16 storage, float32 accumulation, RNE stores */
+} o1d_dtype_t;
+
+typedef enum {
+  O1D_OK = 0,
+  O1D_ERR_INVALID = 1,     /* NULL pointer for a non-empty tensor, negative size, even or non-positive K,
+                              unknown dtype, aliasing output */
+  O1D_ERR_UNSUPPORTED = 2, /* K above O1D_MAX_K, or a size beyond the kernels' 32-bit index range */
+  O1D_ERR_WORKSPACE = 3,   /* workspace smaller than o1d_bwd_weight_workspace_bytes() */
+  O1D_ERR_HIP = 4          /* the HIP runtime rejected a kernel launch */
+} o1d_status_t;
+
+#define O1D_MAX_K 127
+
+/* Forward pass, Definition 1 / Eq. (1): y = conv(x; w, theta). */
+o1d_status_t o1d_fwd(const void* x, const void* w, const float* theta_deg, void* y,
+                     int N, int C, int H, int W, int K, o1d_dtype_t dtype, void* stream);
+
+/* Gradient of Eq. (1) with respect to x (its adjoint in x):
+ *   dx[n,c,h,w] = sum_k w[c,k] * dy[n,c, h - dh_c(k), w - dw_c(k)]   (zero outside the plane).
+ * dx is overwritten, not accumulated. */
+o1d_status_t o1d_bwd_input(const void* dy, const void* w, const float* theta_deg, void* dx,
+                           int N, int C, int H, int W, int K, o1d_dtype_t dtype, void* stream);
+
+/* Gradient of Eq. (1) with respect to w (its adjoint in w):
+ *   dw[c,k] = sum_{n,p,q} dy[n,c,p,q] * x[n,c, p + dh_c(k), q + dw_c(k)]   (zero outside the plane).
+ * dw is overwritten, not accumulated.  `workspace` is caller-owned device
+ * memory of at least o1d_bwd_weight_workspace_bytes(...) bytes (may be NULL
+ * when that size is 0); its contents on entry are ignored and are clobbered.
+ * The reduction order is fixed, so the result is bitwise reproducible. */
+o1d_status_t o1d_bwd_weight(const void* x, const void* dy, const float* theta_deg, void* dw,
+                            int N, int C, int H, int W, int K, o1d_dtype_t dtype,
+                            void* workspace, size_t workspace_bytes, void* stream);
+
+/* Workspace size in bytes that o1d_bwd_weight needs for these sizes. */
+size_t o1d_bwd_weight_workspace_bytes(int N, int C, int H, int W, int K, o1d_dtype_t dtype);
+
+/* Static description of a status code. */
+const char* o1d_status_str(o1d_status_t status);
+
+/* Detail for the calling thread's most recent non-OK status ("" if none). */
+const char* o1d_last_error(void);
+
+/* Library version string. */
+const char* o1d_version(void);
+
+#ifdef __cplusplus
+}
+#endif
+
+#endif /* O1D_H_ */

@@ -1,0 +1,127 @@
+"""Reference oracle for oriented 1D depthwise convolution (CPU, float64).
+
+TEST INFRASTRUCTURE ONLY.  Only the test-suite, the smoke check and the
+benchmark's CPU-baseline leg may import this package.  The library's product
+path never loads it; it shares no code with the HIP kernels.
+
+The arithmetic lives in ``o1d_oracle.c`` (plain C loops, double precision,
+scatter-form backward) and follows Definition 1 / Eq. (1)-(2) of Kirchmeyer &
+Deng, "Convolutional Networks with Oriented 1D Kernels", with pad = K // 2
+placed inside the floor as the appendix section "Padding" requires.  This
+module only compiles it with gcc and marshals numpy arrays through ctypes.
+"""
+from __future__ import annotations
+
+import ctypes
+import os
+import subprocess
+
+import numpy as np
+
+_HERE = os.path.dirname(os.path.abspath(__file__))
+_SRC = os.path.join(_HERE, "o1d_oracle.c")
+_LIB = os.path.join(_HERE, "libo1d_oracle.so")
+_lib = None
+
+_D = ctypes.POINTER(ctypes.c_double)
+_I = ctypes.POINTER(ctypes.c_int)
+
+
+def build(force: bool = True) -> str:
+    """Compile the C oracle into ``oracle/libo1d_oracle.so`` with gcc."""
+    if force or not os.path.exists(_LIB) or os.path.getmtime(_LIB) < os.path.getmtime(_SRC):
+        tmp = _LIB + ".tmp"
+        cmd = ["gcc", "-O2", "-fopenmp", "-fPIC", "-shared", "-std=c99", "-D_GNU_SOURCE",
+               "-o", tmp, _SRC, "-lm"]
+        subprocess.run(cmd, check=True)
+        os.replace(tmp, _LIB)
+    return _LIB
+
+
+def _load():
+    global _lib
+    if _lib is None:
+        if not os.path.exists(_LIB) or os.path.getmtime(_LIB) < os.path.getmtime(_SRC):
+            build(force=True)
+        lib = ctypes.CDLL(_LIB)
+        lib.oracle_offsets_real.argtypes = [ctypes.c_double, ctypes.c_int, ctypes.c_int, _D, _D]
+        lib.oracle_offsets_real.restype = None
+        lib.oracle_offsets.argtypes = [ctypes.c_double, ctypes.c_int, ctypes.c_int, _I, _I]
+        lib.oracle_offsets.restype = None
+        for name in ("oracle_fwd", "oracle_bwd_input", "oracle_bwd_weight"):
+            f = getattr(lib, name)
+            f.argtypes = [_D, _D, _D, _D] + [ctypes.c_int] * 6
+            f.restype = None
+        _lib = lib
+    return _lib
+
+
+def _f64(a) -> np.ndarray:
+    return np.ascontiguousarray(np.asarray(a, dtype=np.float64))
+
+
+def _ptr(a: np.ndarray, t=_D):
+    return a.ctypes.data_as(t)
+
+
+def default_threads() -> int:
+    return max(1, len(os.sched_getaffinity(0)))
+
+
+def offsets_real(theta_deg: float, K: int, pad: int | None = None):
+    """Unrounded filter offsets (dh, dw) = R_theta (0, k - pad)^T for k < K."""
+    lib = _load()
+    pad = K // 2 if pad is None else pad
+    vh = np.zeros(K, np.float64)
+    vw = np.zeros(K, np.float64)
+    lib.oracle_offsets_real(float(theta_deg), K, pad, _ptr(vh), _ptr(vw))
+    return vh, vw
+
+
+def offsets(theta_deg: float, K: int, pad: int | None = None):
+    """Integer filter offsets floor(R_theta (0, k - pad)^T) (Eq. 2)."""
+    lib = _load()
+    pad = K // 2 if pad is None else pad
+    dh = np.zeros(K, np.int32)
+    dw = np.zeros(K, np.int32)
+    lib.oracle_offsets(float(theta_deg), K, pad, _ptr(dh, _I), _ptr(dw, _I))
+    return dh, dw
+
+
+def _check(x, K, C):
+    if x.ndim != 4:
+        raise ValueError("expected an NCHW array")
+    if K < 1 or K % 2 == 0:
+        raise ValueError("K must be odd and positive")
+
+
+def fwd(x, w, theta_deg, threads: int | None = None) -> np.ndarray:
+    """y = oriented depthwise 1D convolution of x (N,C,H,W) with w (C,K)."""
+    x = _f64(x); w = _f64(w); th = _f64(theta_deg)
+    N, C, H, W = x.shape
+    K = w.shape[1]
+    _check(x, K, C)
+    y = np.empty_like(x)
+    _load().oracle_fwd(_ptr(x), _ptr(w), _ptr(th), _ptr(y), N, C, H, W, K, threads or default_threads())
+    return y
+
+
+def bwd_input(dy, w, theta_deg, threads: int | None = None) -> np.ndarray:
+    """dL/dx given dL/dy (scatter form of the adjoint of Eq. 1)."""
+    dy = _f64(dy); w = _f64(w); th = _f64(theta_deg)
+    N, C, H, W = dy.shape
+    K = w.shape[1]
+    _check(dy, K, C)
+    dx = np.empty_like(dy)
+    _load().oracle_bwd_input(_ptr(dy), _ptr(w), _ptr(th), _ptr(dx), N, C, H, W, K, threads or default_threads())
+    return dx
+
+
+def bwd_weight(x, dy, theta_deg, K: int, threads: int | None = None) -> np.ndarray:
+    """dL/dw (C,K) given the input x and dL/dy (scatter form of the adjoint of Eq. 1)."""
+    x = _f64(x); dy = _f64(dy); th = _f64(theta_deg)
+    N, C, H, W = x.shape
+    _check(x, K, C)
+    dw = np.empty((C, K), np.float64)
+    _load().oracle_bwd_weight(_ptr(x), _ptr(dy), _ptr(th), _ptr(dw), N, C, H, W, K, threads or default_threads())
+    return dw
