@@ -1,0 +1,132 @@
+// C ABI of the oriented 1D depthwise convolution library (declared in
+// include/o1d.h): argument validation, status codes, per-thread error text
+// and dispatch to the kernel launchers.  No device memory is allocated here.
+#include <hip/hip_runtime.h>
+#include <stdarg.h>
+#include <stdint.h>
+#include <stdio.h>
+
+#include "o1d.h"
+#include "o1d_launch.h"
+#include "o1d_plan.h"
+
+namespace {
+
+thread_local char g_last_error[512] = "";
+
+o1d_status_t fail(o1d_status_t st, const char* fmt, ...) {
+  va_list ap;
+  va_start(ap, fmt);
+  vsnprintf(g_last_error, sizeof(g_last_error), fmt, ap);
+  va_end(ap);
+  return st;
+}
+
+o1d_status_t ok() {
+  g_last_error[0] = '\0';
+  return O1D_OK;
+}
+
+size_t elem_size(o1d_dtype_t dt) { return dt == O1D_BF16 ? 2u : 4u; }
+
+bool overlaps(const void* a, size_t abytes, const void* b, size_t bbytes) {
+  const uintptr_t a0 = (uintptr_t)a, b0 = (uintptr_t)b;
+  return a0 < b0 + bbytes && b0 < a0 + abytes;
+}
+
+// Checks shared by all entry points.  Sets *empty when there is nothing to
+// compute over the batch/plane (N, H or W zero) or no channel (C zero).
+o1d_status_t check_sizes(const char* fn, int N, int C, int H, int W, int K, o1d_dtype_t dt) {
+  if (dt != O1D_F32 && dt != O1D_BF16) return fail(O1D_ERR_INVALID, "%s: unknown dtype %d", fn, (int)dt);
+  if (N < 0 || C < 0 || H < 0 || W < 0)
+    return fail(O1D_ERR_INVALID, "%s: negative size N=%d C=%d H=%d W=%d", fn, N, C, H, W);
+  if (K < 1 || (K % 2) == 0)
+    return fail(O1D_ERR_INVALID, "%s: K=%d must be odd and positive (pad = K/2 centres the kernel)", fn, K);
+  if (K > O1D_MAX_K) return fail(O1D_ERR_UNSUPPORTED, "%s: K=%d exceeds O1D_MAX_K=%d", fn, K, O1D_MAX_K);
+  if (C > 65535 || N > 65535)
+    return fail(O1D_ERR_UNSUPPORTED, "%s: N=%d or C=%d exceeds the 65535 grid limit", fn, N, C);
+  if ((long long)H * (long long)W > (1ll << 30))
+    return fail(O1D_ERR_UNSUPPORTED, "%s: plane %dx%d exceeds 2^30 elements", fn, H, W);
+  return O1D_OK;
+}
+
+o1d_status_t hip_status(const char* fn, hipError_t e) {
+  if (e != hipSuccess) return fail(O1D_ERR_HIP, "%s: kernel launch failed: %s", fn, hipGetErrorString(e));
+  return ok();
+}
+
+o1d_status_t gather_entry(const char* fn, const void* in, const void* w, const float* theta, void* out, int N, int C,
+                          int H, int W, int K, o1d_dtype_t dt, void* stream, int sign) {
+  o1d_status_t st = check_sizes(fn, N, C, H, W, K, dt);
+  if (st != O1D_OK) return st;
+  const size_t elems = (size_t)N * C * H * W;
+  if (elems == 0) return ok();
+  if (!in || !w || !theta || !out) return fail(O1D_ERR_INVALID, "%s: NULL tensor pointer", fn);
+  const size_t bytes = elems * elem_size(dt);
+  if (overlaps(in, bytes, out, bytes)) return fail(O1D_ERR_INVALID, "%s: output overlaps input", fn);
+  (void)hipGetLastError();
+  return hip_status(fn, o1d::launch_gather((o1d::Dtype)dt, in, w, theta, out, N, C, H, W, K, sign,
+                                           static_cast<hipStream_t>(stream)));
+}
+
+}  // namespace
+
+extern "C" {
+
+size_t o1d_bwd_weight_workspace_bytes(int N, int C, int H, int W, int K, o1d_dtype_t dtype) {
+  if (check_sizes("o1d_bwd_weight_workspace_bytes", N, C, H, W, K, dtype) != O1D_OK) return 0;
+  if ((size_t)N * C * H * W == 0) return 0;
+  const o1d::WgradPlan p = o1d::plan_wgrad(N, C, H, W, K);
+  return p.parts() * (size_t)C * (size_t)K * sizeof(float);
+}
+
+o1d_status_t o1d_fwd(const void* x, const void* w, const float* theta_deg, void* y, int N, int C, int H, int W, int K,
+                     o1d_dtype_t dtype, void* stream) {
+  return gather_entry("o1d_fwd", x, w, theta_deg, y, N, C, H, W, K, dtype, stream, +1);
+}
+
+o1d_status_t o1d_bwd_input(const void* dy, const void* w, const float* theta_deg, void* dx, int N, int C, int H,
+                           int W, int K, o1d_dtype_t dtype, void* stream) {
+  return gather_entry("o1d_bwd_input", dy, w, theta_deg, dx, N, C, H, W, K, dtype, stream, -1);
+}
+
+o1d_status_t o1d_bwd_weight(const void* x, const void* dy, const float* theta_deg, void* dw, int N, int C, int H,
+                            int W, int K, o1d_dtype_t dtype, void* workspace, size_t workspace_bytes, void* stream) {
+  const char* fn = "o1d_bwd_weight";
+  o1d_status_t st = check_sizes(fn, N, C, H, W, K, dtype);
+  if (st != O1D_OK) return st;
+  if (C == 0) return ok();
+  if (!dw) return fail(O1D_ERR_INVALID, "%s: NULL dw pointer", fn);
+  hipStream_t s = static_cast<hipStream_t>(stream);
+  const size_t elems = (size_t)N * C * H * W;
+  (void)hipGetLastError();
+  if (elems == 0) return hip_status(fn, o1d::launch_zero((o1d::Dtype)dtype, dw, (size_t)C * K, s));
+  if (!x || !dy || !theta_deg) return fail(O1D_ERR_INVALID, "%s: NULL tensor pointer", fn);
+  const size_t need = o1d_bwd_weight_workspace_bytes(N, C, H, W, K, dtype);
+  if (workspace_bytes < need || (need > 0 && !workspace))
+    return fail(O1D_ERR_WORKSPACE, "%s: workspace of %zu bytes given, %zu needed", fn, workspace_bytes, need);
+  const size_t dwbytes = (size_t)C * K * elem_size(dtype), tbytes = elems * elem_size(dtype);
+  if (overlaps(dw, dwbytes, x, tbytes) || overlaps(dw, dwbytes, dy, tbytes) ||
+      (need > 0 && (overlaps(workspace, need, x, tbytes) || overlaps(workspace, need, dy, tbytes) ||
+                    overlaps(workspace, need, dw, dwbytes))))
+    return fail(O1D_ERR_INVALID, "%s: dw or workspace overlaps an input", fn);
+  return hip_status(fn, o1d::launch_wgrad((o1d::Dtype)dtype, x, dy, theta_deg, dw, static_cast<float*>(workspace), N,
+                                          C, H, W, K, s));
+}
+
+const char* o1d_status_str(o1d_status_t status) {
+  switch (status) {
+    case O1D_OK: return "O1D_OK";
+    case O1D_ERR_INVALID: return "O1D_ERR_INVALID: invalid argument";
+    case O1D_ERR_UNSUPPORTED: return "O1D_ERR_UNSUPPORTED: size outside the supported range";
+    case O1D_ERR_WORKSPACE: return "O1D_ERR_WORKSPACE: workspace too small";
+    case O1D_ERR_HIP: return "O1D_ERR_HIP: HIP runtime error";
+  }
+  return "unknown o1d status";
+}
+
+const char* o1d_last_error(void) { return g_last_error; }
+
+const char* o1d_version(void) { return "o1d 0.1.0 (gfx950)"; }
+
+}  // extern "C"

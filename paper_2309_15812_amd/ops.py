@@ -1,0 +1,96 @@
+"""torch-facing wrappers of the C ABI: tensors in, tensors out.
+
+PyTorch supplies device memory and the current stream; the three entry points
+below only check shapes, allocate outputs and hand raw pointers to
+libo1d.so.  theta is a float32 tensor of per-channel angles in degrees.
+"""
+from __future__ import annotations
+
+import torch
+
+from . import _lib
+
+_DT = {torch.float32: _lib.O1D_F32, torch.bfloat16: _lib.O1D_BF16}
+
+
+def _stream(t: torch.Tensor) -> int:
+    return torch.cuda.current_stream(t.device).cuda_stream
+
+
+def _dt(t: torch.Tensor) -> int:
+    if t.dtype not in _DT:
+        raise TypeError(f"unsupported dtype {t.dtype}; use float32 or bfloat16")
+    return _DT[t.dtype]
+
+
+def _check_common(x: torch.Tensor, w: torch.Tensor, theta: torch.Tensor):
+    if x.dim() != 4 or w.dim() != 2:
+        raise ValueError("expected x as (N, C, H, W) and w as (C, K)")
+    N, C, H, W = x.shape
+    if w.shape[0] != C or theta.shape != (C,):
+        raise ValueError(f"w {tuple(w.shape)} / theta {tuple(theta.shape)} do not match C={C}")
+    if w.dtype != x.dtype:
+        raise TypeError("x and w must share a dtype")
+    if theta.dtype != torch.float32:
+        raise TypeError("theta must be float32 degrees")
+    for t in (x, w, theta):
+        if not t.is_cuda or not t.is_contiguous():
+            raise ValueError("tensors must be contiguous and on the GPU")
+    return N, C, H, W, int(w.shape[1])
+
+
+def fwd(x: torch.Tensor, w: torch.Tensor, theta: torch.Tensor, out: torch.Tensor | None = None) -> torch.Tensor:
+    """y = oriented depthwise 1D convolution of x (Definition 1, Eq. 1-2)."""
+    N, C, H, W, K = _check_common(x, w, theta)
+    y = torch.empty_like(x) if out is None else out
+    _lib.check("o1d_fwd", _lib.call("o1d_fwd", x.data_ptr(), w.data_ptr(), theta.data_ptr(), y.data_ptr(),
+                                    N, C, H, W, K, _dt(x), _stream(x)))
+    return y
+
+
+def bwd_input(dy: torch.Tensor, w: torch.Tensor, theta: torch.Tensor, out: torch.Tensor | None = None) -> torch.Tensor:
+    """dx given dy (adjoint of Eq. 1 in x)."""
+    N, C, H, W, K = _check_common(dy, w, theta)
+    dx = torch.empty_like(dy) if out is None else out
+    _lib.check("o1d_bwd_input", _lib.call("o1d_bwd_input", dy.data_ptr(), w.data_ptr(), theta.data_ptr(),
+                                          dx.data_ptr(), N, C, H, W, K, _dt(dy), _stream(dy)))
+    return dx
+
+
+def workspace_bytes(N: int, C: int, H: int, W: int, K: int, dtype: torch.dtype) -> int:
+    return int(_lib.lib().o1d_bwd_weight_workspace_bytes(N, C, H, W, K, _DT[dtype]))
+
+
+def bwd_weight(x: torch.Tensor, dy: torch.Tensor, theta: torch.Tensor, K: int, out: torch.Tensor | None = None,
+               workspace: torch.Tensor | None = None) -> torch.Tensor:
+    """dw (C, K) given x and dy (adjoint of Eq. 1 in w)."""
+    if dy.shape != x.shape or dy.dtype != x.dtype:
+        raise ValueError("x and dy must have the same shape and dtype")
+    N, C, H, W = x.shape
+    dw = torch.empty((C, K), dtype=x.dtype, device=x.device) if out is None else out
+    _check_common(x, dw, theta)
+    need = workspace_bytes(N, C, H, W, K, x.dtype)
+    if workspace is None:
+        workspace = torch.empty(max(need, 1), dtype=torch.uint8, device=x.device)
+    nbytes = workspace.numel() * workspace.element_size()
+    _lib.check("o1d_bwd_weight", _lib.call("o1d_bwd_weight", x.data_ptr(), dy.data_ptr(), theta.data_ptr(),
+                                           dw.data_ptr(), N, C, H, W, K, _dt(x), workspace.data_ptr(), nbytes,
+                                           _stream(x)))
+    return dw
+
+
+class OrientedConv1dFunction(torch.autograd.Function):
+    """Autograd glue: forward -> o1d_fwd, backward -> o1d_bwd_input + o1d_bwd_weight (theta gets no gradient)."""
+
+    @staticmethod
+    def forward(ctx, x, w, theta):
+        ctx.save_for_backward(x, w, theta)
+        return fwd(x.contiguous(), w.contiguous(), theta.contiguous())
+
+    @staticmethod
+    def backward(ctx, gy):
+        x, w, theta = ctx.saved_tensors
+        gy = gy.contiguous()
+        gx = bwd_input(gy, w, theta) if ctx.needs_input_grad[0] else None
+        gw = bwd_weight(x, gy, theta, w.shape[1]) if ctx.needs_input_grad[1] else None
+        return gx, gw, None
