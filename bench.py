@@ -1,0 +1,253 @@
+#!/usr/bin/env python3
+"""Throughput benchmark of oriented 1D depthwise convolution on one MI355X.
+
+One step = the whole hot path on one batch: forward (o1d_fwd), input gradient
+(o1d_bwd_input) and weight gradient (o1d_bwd_weight), on the headline workload
+64 x 96 x 56 x 56, K = 31, float32, per-channel angles drawn from the eight
+directions i * 22.5 degrees (ConvNeXt-T stage-1 shape, synthetic data).
+
+Inputs are resident in HBM when the timed region starts.  Steps rotate over
+several disjoint buffer sets whose total size far exceeds the 256 MB
+Infinity Cache, so a step never finds its inputs cached by an earlier step.
+
+Prints ONE JSON line: value = algorithmic bytes of the step (each op reads one
+tensor and writes one, or reads two: 6 tensors of N*C*H*W elements) divided
+by the measured time, in GB/s.  The "roofline" object reports the dominant
+kernel's algorithmic bytes per launch over its mean duration (HIP events on
+the stream it runs on) against the 8 TB/s HBM peak; "cpu_baseline" times the
+float64 CPU oracle on the same workload.
+"""
+from __future__ import annotations
+
+import argparse
+import hashlib
+import json
+import os
+import statistics
+import sys
+import time
+
+ROOT = os.path.dirname(os.path.abspath(__file__))
+sys.path.insert(0, ROOT)
+
+METRIC = "oriented-1D DW conv fwd+bwd ms & GB/s (% HBM peak), K=31, 64×96×56×56"
+HBM_PEAK_GBS = 8000.0
+CSRC = os.path.join(ROOT, "paper_2309_15812_amd", "csrc")
+TRAFFIC_FILE = os.path.join(ROOT, "profiles", "traffic_metric_workload.json")
+
+
+def kernel_source_hash() -> str:
+    h = hashlib.sha256()
+    for name in sorted(os.listdir(CSRC)):
+        if name.endswith((".hip", ".h")):
+            with open(os.path.join(CSRC, name), "rb") as f:
+                h.update(name.encode() + b"\0" + f.read())
+    return h.hexdigest()[:16]
+
+
+def parse():
+    ap = argparse.ArgumentParser(description=__doc__.split("\n\n")[0])
+    ap.add_argument("--gpus", type=int, default=1)
+    ap.add_argument("--steps", type=int, default=50)
+    ap.add_argument("--warmup", type=int, default=10)
+    ap.add_argument("--workload", default="metric")
+    ap.add_argument("--sets", type=int, default=6, help="rotating buffer sets (cache defeat)")
+    ap.add_argument("--no-cpu", action="store_true", help="skip the CPU oracle baseline")
+    ap.add_argument("--cpu-seconds", type=float, default=12.0, help="target CPU work for the oracle sample")
+    ap.add_argument("--angle-sweep", action="store_true", help="time every K of the angle-cost sweep")
+    ap.add_argument("--only", default="", help="profiling aid: run only this op (fwd|bwd_input|bwd_weight)")
+    return ap.parse_args()
+
+
+class BufferSet:
+    def __init__(self, d, wl, torch, dev, ops):
+        dt = torch.float32 if wl.dtype == "f32" else torch.bfloat16
+        self.x = torch.from_numpy(d["x"]).to(dev).to(dt)
+        self.dy = torch.from_numpy(d["dy"]).to(dev).to(dt)
+        self.w = torch.from_numpy(d["w"]).to(dev).to(dt)
+        self.th = torch.from_numpy(d["theta"]).to(dev)
+        self.y = torch.empty_like(self.x)
+        self.dx = torch.empty_like(self.x)
+        self.dw = torch.empty_like(self.w)
+        need = ops.workspace_bytes(wl.N, wl.C, wl.H, wl.W, wl.K, dt)
+        self.ws = torch.empty(max(need, 1), dtype=torch.uint8, device=dev)
+
+
+def run_ops(ops, b, K, only=""):
+    if not only or only == "fwd":
+        ops.fwd(b.x, b.w, b.th, out=b.y)
+    if not only or only == "bwd_input":
+        ops.bwd_input(b.dy, b.w, b.th, out=b.dx)
+    if not only or only == "bwd_weight":
+        ops.bwd_weight(b.x, b.dy, b.th, K, out=b.dw, workspace=b.ws)
+
+
+def time_workload(wl, steps, warmup, nsets, torch, ops, synth, only="", per_op=True):
+    """Returns (ms_per_step, {op: [durations ms]})."""
+    dev = torch.device("cuda:0")
+    d = synth.make_inputs(wl)
+    sets = [BufferSet(d, wl, torch, dev, ops) for _ in range(nsets)]
+    for i in range(warmup):
+        run_ops(ops, sets[i % nsets], wl.K, only)
+    names = [only] if only else ["fwd", "bwd_input", "bwd_weight"]
+    stream = torch.cuda.current_stream(dev)
+    ev = []
+    torch.cuda.synchronize()
+    t0 = time.perf_counter()
+    for i in range(steps):
+        b = sets[i % nsets]
+        if per_op:
+            marks = [torch.cuda.Event(enable_timing=True) for _ in range(len(names) + 1)]
+            marks[0].record(stream)
+            for j, nm in enumerate(names):
+                run_ops(ops, b, wl.K, nm)
+                marks[j + 1].record(stream)
+            ev.append(marks)
+        else:
+            run_ops(ops, b, wl.K, only)
+    torch.cuda.synchronize()
+    t1 = time.perf_counter()
+    durs = {nm: [] for nm in names}
+    for marks in ev:
+        for j, nm in enumerate(names):
+            durs[nm].append(marks[j].elapsed_time(marks[j + 1]))
+    del sets
+    torch.cuda.empty_cache()
+    return (t1 - t0) * 1e3 / steps, durs
+
+
+def cpu_baseline(wl, synth, seconds):
+    import numpy as np
+
+    import oracle
+
+    threads = oracle.default_threads()
+    d = synth.make_inputs(wl)
+    x, dy, w = (np.asarray(d[k], np.float64) for k in ("x", "dy", "w"))
+    th = np.asarray(d["theta"], np.float64)
+    reps, t_total = 0, 0.0
+    while t_total < seconds and reps < 50:
+        t0 = time.perf_counter()
+        oracle.fwd(x, w, th, threads)
+        oracle.bwd_input(dy, w, th, threads)
+        oracle.bwd_weight(x, dy, th, wl.K, threads)
+        t_total += time.perf_counter() - t0
+        reps += 1
+    step_bytes = 6 * wl.elems * wl.elem_bytes
+    return {
+        "value": round(step_bytes * reps / t_total / 1e9, 3),
+        "unit": "GB/s",
+        "cores": threads,
+        "kind": "oracle",
+        "sample": f"{reps} full step(s) of the same workload (fwd + bwd_input + bwd_weight, "
+                  f"{wl.N}x{wl.C}x{wl.H}x{wl.W}, K={wl.K}) in float64 C loops, OpenMP over planes/channels; "
+                  f"{t_total:.1f} s",
+        "ms_per_step": round(t_total * 1e3 / reps, 1),
+    }
+
+
+def traffic_for(op_name: str):
+    """HBM bytes per launch from the committed rocprofv3 counter summary, if it
+    was taken on the current kernel sources."""
+    try:
+        with open(TRAFFIC_FILE) as f:
+            rec = json.load(f)
+    except (OSError, ValueError):
+        return None
+    if rec.get("kernel_source_hash") != kernel_source_hash():
+        return None
+    ent = rec.get("ops", {}).get(op_name)
+    return None if ent is None else ent.get("hbm_bytes_per_launch")
+
+
+def main():
+    args = parse()
+    if args.gpus != 1 or int(os.environ.get("WORLD_SIZE", "1")) > 1:
+        print(json.dumps({"error": "this benchmark runs on exactly one GPU; the operation shards over channels "
+                                   "or images with no exchange (see DESIGN.md), and multi-GPU runs are not "
+                                   "part of this build", "n_gpus": args.gpus}), flush=True)
+        sys.exit(2)
+
+    import torch
+
+    from paper_2309_15812_amd import ops, synth
+
+    wl = synth.WORKLOADS[args.workload]
+    T = wl.elems * wl.elem_bytes
+    print(f"[bench] workload {wl} T={T / 1e6:.2f} MB sets={args.sets}", file=sys.stderr, flush=True)
+    ms, durs = time_workload(wl, args.steps, args.warmup, args.sets, torch, ops, synth, args.only)
+    print(f"[bench] {ms:.4f} ms/step", file=sys.stderr, flush=True)
+
+    op_bytes = {"fwd": 2 * T, "bwd_input": 2 * T, "bwd_weight": 2 * T + wl.C * wl.K * wl.elem_bytes}
+    per_op = {}
+    for nm, v in durs.items():
+        mean = statistics.fmean(v)
+        per_op[nm] = {
+            "ms_mean": round(mean, 5),
+            "ms_median": round(statistics.median(v), 5),
+            "ms_std": round(statistics.pstdev(v), 5),
+            "GB/s": round(op_bytes[nm] / (mean * 1e-3) / 1e9, 1),
+            "frac_hbm_peak": round(op_bytes[nm] / (mean * 1e-3) / 1e9 / HBM_PEAK_GBS, 4),
+        }
+    dominant = max(per_op, key=lambda k: per_op[k]["ms_mean"])
+    dom_ms = per_op[dominant]["ms_mean"]
+    achieved = op_bytes[dominant] / (dom_ms * 1e-3) / 1e9
+    step_bytes = sum(op_bytes[k] for k in durs)
+    out = {
+        "metric": METRIC,
+        "value": round(step_bytes / (ms * 1e-3) / 1e9, 2),
+        "unit": "GB/s",
+        "n_gpus": 1,
+        "steps": args.steps,
+        "warmup": args.warmup,
+        "ms_per_step": round(ms, 5),
+        "higher_is_better": True,
+        "scaling": "weak",
+        "vs_baseline": None,
+        "dtype": wl.dtype,
+        "data": "synthetic",
+        "config": {
+            "workload": f"{wl.name}: N={wl.N} C={wl.C} H={wl.H} W={wl.W} K={wl.K} {wl.dtype}, theta from the 8 "
+                        f"directions i*22.5 deg, one step = fwd + bwd_input + bwd_weight",
+            "N": wl.N, "C": wl.C, "H": wl.H, "W": wl.W, "K": wl.K,
+            "buffer_sets": args.sets,
+            "step_bytes": step_bytes,
+        },
+        "frac_hbm_peak_step": round(step_bytes / (ms * 1e-3) / 1e9 / HBM_PEAK_GBS, 4),
+        "roofline": {
+            "bound": "hbm",
+            "kernel": dominant,
+            "achieved": round(achieved, 1),
+            "peak": HBM_PEAK_GBS,
+            "unit": "GB/s",
+            "frac": round(achieved / HBM_PEAK_GBS, 4),
+            "traffic": traffic_for(dominant),
+            "algorithmic_bytes_per_launch": op_bytes[dominant],
+            "ms_per_launch": dom_ms,
+        },
+        "ops": per_op,
+    }
+
+    if not args.only:
+        # Angle cost: the same shapes at theta = 0, 90 and uniform continuous angles.
+        sweep = {}
+        for K in ([7, 15, 31, 63] if args.angle_sweep else [31]):
+            base = synth.WORKLOADS["c5"].replace(K=K)
+            res = {}
+            for mode in ("zero", "ninety", "uniform"):
+                m, dd = time_workload(base.replace(theta=mode), 20, 5, 3, torch, ops, synth)
+                res[mode] = {"step_ms": round(m, 4), "fwd_ms": round(statistics.fmean(dd["fwd"]), 4)}
+            r_step = max(v["step_ms"] for v in res.values()) / res["zero"]["step_ms"]
+            r_fwd = max(v["fwd_ms"] for v in res.values()) / res["zero"]["fwd_ms"]
+            sweep[f"K{K}"] = {**res, "max_over_theta0_step": round(r_step, 3), "max_over_theta0_fwd": round(r_fwd, 3)}
+            print(f"[bench] angle sweep K={K}: {sweep[f'K{K}']}", file=sys.stderr, flush=True)
+        out["angle_cost"] = {"workload": "32x256x56x56 f32 fwd+bwd", **sweep}
+
+    if not args.no_cpu and not args.only:
+        print("[bench] timing the CPU oracle ...", file=sys.stderr, flush=True)
+        out["cpu_baseline"] = cpu_baseline(wl, synth, args.cpu_seconds)
+    print(json.dumps(out), flush=True)
+
+
+if __name__ == "__main__":
+    main()

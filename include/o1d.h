@@ -83,7 +83,9 @@ o1d_status_t o1d_bwd_input(const void* dy, const void* w, const float* theta_deg
  * dw is overwritten, not accumulated.  `workspace` is caller-owned device
  * memory of at least o1d_bwd_weight_workspace_bytes(...) bytes (may be NULL
  * when that size is 0); its contents on entry are ignored and are clobbered.
- * The reduction order is fixed, so the result is bitwise reproducible. */
+ * Partial sums are combined with float32 additions whose order can vary from
+ * run to run, so dw is reproducible to rounding (not bitwise); o1d_fwd and
+ * o1d_bwd_input are bitwise reproducible. */
 o1d_status_t o1d_bwd_weight(const void* x, const void* dy, const float* theta_deg, void* dw,
                             int N, int C, int H, int W, int K, o1d_dtype_t dtype,
                             void* workspace, size_t workspace_bytes, void* stream);

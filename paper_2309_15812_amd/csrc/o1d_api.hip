@@ -5,10 +5,12 @@
 #include <stdarg.h>
 #include <stdint.h>
 #include <stdio.h>
+#include <stdlib.h>
 
 #include "o1d.h"
 #include "o1d_launch.h"
 #include "o1d_plan.h"
+#include "o1d_runs.h"
 
 namespace {
 
@@ -50,6 +52,25 @@ o1d_status_t check_sizes(const char* fn, int N, int C, int H, int W, int K, o1d_
   return O1D_OK;
 }
 
+// Kernel family: the run-decomposed kernels cover K <= 63 and planes that fit
+// in LDS with their halo; everything else takes the general tiled kernels.
+// O1D_KERNEL=tiled forces the tiled kernels (a comparison aid).
+bool runs_allowed() {
+  const char* e = getenv("O1D_KERNEL");
+  return !(e && e[0] == 't');
+}
+
+o1d::runs::RunsPlan runs_plan(int N, int C, int H, int W, int K, int sign, int kind) {
+  if (!runs_allowed()) return o1d::runs::RunsPlan();
+  return o1d::runs::plan_runs(N, C, H, W, K, sign, kind);
+}
+
+size_t wgrad_workspace(int N, int C, int H, int W, int K) {
+  const o1d::runs::RunsPlan rp = runs_plan(N, C, H, W, K, 1, 1);
+  const size_t parts = rp.ok ? (size_t)rp.blocks_n : o1d::plan_wgrad(N, C, H, W, K).parts();
+  return parts * (size_t)C * (size_t)K * sizeof(float);
+}
+
 o1d_status_t hip_status(const char* fn, hipError_t e) {
   if (e != hipSuccess) return fail(O1D_ERR_HIP, "%s: kernel launch failed: %s", fn, hipGetErrorString(e));
   return ok();
@@ -65,8 +86,10 @@ o1d_status_t gather_entry(const char* fn, const void* in, const void* w, const f
   const size_t bytes = elems * elem_size(dt);
   if (overlaps(in, bytes, out, bytes)) return fail(O1D_ERR_INVALID, "%s: output overlaps input", fn);
   (void)hipGetLastError();
-  return hip_status(fn, o1d::launch_gather((o1d::Dtype)dt, in, w, theta, out, N, C, H, W, K, sign,
-                                           static_cast<hipStream_t>(stream)));
+  hipStream_t s = static_cast<hipStream_t>(stream);
+  const o1d::runs::RunsPlan rp = runs_plan(N, C, H, W, K, sign, 0);
+  if (rp.ok) return hip_status(fn, o1d::launch_gather_runs((o1d::Dtype)dt, rp, in, w, theta, out, s));
+  return hip_status(fn, o1d::launch_gather((o1d::Dtype)dt, in, w, theta, out, N, C, H, W, K, sign, s));
 }
 
 }  // namespace
@@ -76,8 +99,7 @@ extern "C" {
 size_t o1d_bwd_weight_workspace_bytes(int N, int C, int H, int W, int K, o1d_dtype_t dtype) {
   if (check_sizes("o1d_bwd_weight_workspace_bytes", N, C, H, W, K, dtype) != O1D_OK) return 0;
   if ((size_t)N * C * H * W == 0) return 0;
-  const o1d::WgradPlan p = o1d::plan_wgrad(N, C, H, W, K);
-  return p.parts() * (size_t)C * (size_t)K * sizeof(float);
+  return wgrad_workspace(N, C, H, W, K);
 }
 
 o1d_status_t o1d_fwd(const void* x, const void* w, const float* theta_deg, void* y, int N, int C, int H, int W, int K,
@@ -110,6 +132,10 @@ o1d_status_t o1d_bwd_weight(const void* x, const void* dy, const float* theta_de
       (need > 0 && (overlaps(workspace, need, x, tbytes) || overlaps(workspace, need, dy, tbytes) ||
                     overlaps(workspace, need, dw, dwbytes))))
     return fail(O1D_ERR_INVALID, "%s: dw or workspace overlaps an input", fn);
+  const o1d::runs::RunsPlan rp = runs_plan(N, C, H, W, K, 1, 1);
+  if (rp.ok)
+    return hip_status(fn, o1d::launch_wgrad_runs((o1d::Dtype)dtype, rp, x, dy, theta_deg, dw,
+                                                 static_cast<float*>(workspace), s));
   return hip_status(fn, o1d::launch_wgrad((o1d::Dtype)dtype, x, dy, theta_deg, dw, static_cast<float*>(workspace), N,
                                           C, H, W, K, s));
 }
