@@ -83,9 +83,8 @@ o1d_status_t o1d_bwd_input(const void* dy, const void* w, const float* theta_deg
  * dw is overwritten, not accumulated.  `workspace` is caller-owned device
  * memory of at least o1d_bwd_weight_workspace_bytes(...) bytes (may be NULL
  * when that size is 0); its contents on entry are ignored and are clobbered.
- * Partial sums are combined with float32 additions whose order can vary from
- * run to run, so dw is reproducible to rounding (not bitwise); o1d_fwd and
- * o1d_bwd_input are bitwise reproducible. */
+ * Partial sums are combined in a fixed order, so dw (like the outputs of
+ * o1d_fwd and o1d_bwd_input) is bitwise reproducible for the same inputs. */
 o1d_status_t o1d_bwd_weight(const void* x, const void* dy, const float* theta_deg, void* dw,
                             int N, int C, int H, int W, int K, o1d_dtype_t dtype,
                             void* workspace, size_t workspace_bytes, void* stream);

@@ -19,7 +19,7 @@ constexpr int kMaxTaps = 64;    // K <= 63: one tap per lane of wave 0
 constexpr int kMaxRuns = 64;
 constexpr int kThreads2 = 512;  // 8 waves per workgroup
 constexpr int kMaxStage = 8;    // staged elements per thread per plane group
-constexpr int kProgBytes = 4 * (8 + 4 * 64) + 4 * 64 * 8;  // matches sizeof(Prog) in o1d_runs.hip
+constexpr int kProgBytes = 4 * (16 + 4 * 64) + 4 * 64 * 8;  // matches sizeof(Prog) in o1d_runs.hip
 
 // Row strides compiled into the kernels.  A wave-tile is RB bands x CB
 // columns of strips (RB * CB = 64 lanes); its lanes hit distinct LDS banks
@@ -83,7 +83,7 @@ inline RunsPlan plan_runs(int N, int C, int H, int W, int K, int sign, int kind)
   const size_t budget = 56 * 1024;
   auto lds_for = [&](int g) -> size_t {
     size_t f = (size_t)kProgBytes / 4 + (size_t)g * p.PS;
-    if (kind == 1) f += (size_t)K * 64 + (size_t)g * HW;
+    if (kind == 1) f += 8 * 64 + (((size_t)g * HW + 3) & ~(size_t)3);
     return f * 4;
   };
   while (G > 1 && lds_for(G) > budget) --G;

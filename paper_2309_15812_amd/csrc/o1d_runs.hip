@@ -47,10 +47,11 @@ struct Prog {
   int transposed;  // staging frame = transposed plane
   int finite;      // the channel's angle is finite
   int pad_[3];
+  int group[8];            // runs of length L occupy [group[L-1], group[L]) (group[0] = 0)
   int run_off[kMaxRuns];   // LDS offset of the run's first cell (along +u) from the output pixel
-  int run_len[kMaxRuns];
-  int run_slot[kMaxRuns];  // first cell slot of the run (weight-gradient accumulators)
-  int tap_slot[kMaxTaps];  // cell slot of every tap (duplicate taps share one)
+  int cell_off[kMaxTaps];  // LDS offset of every distinct cell (cell order)
+  int tap_cell[kMaxTaps];  // cell of every tap (duplicate taps share one)
+  int pad2_[64];
   float run_w[kMaxRuns * 8];
 };
 static_assert(sizeof(Prog) == kProgBytes, "kProgBytes must match the program layout");
@@ -74,9 +75,11 @@ __device__ __forceinline__ int hibit(uint64_t m) { return 63 - __clzll(m); }
 __device__ __forceinline__ int lobit(uint64_t m) { return __ffsll((long long)m) - 1; }
 
 // Builds the channel's program; called by all 64 lanes of wave 0 (K <= 63).
-// `sign` = -1 negates the cells (input gradient).
+// `sign` = -1 negates the cells (input gradient); `allow_transpose` = false
+// keeps the plane's own frame (the weight gradient does not use runs).
 template <typename T, int S>
-__device__ void build_program(Prog* pg, const T* __restrict__ wgt, float theta, int c, int K, int sign) {
+__device__ void build_program(Prog* pg, const T* __restrict__ wgt, float theta, int c, int K, int sign,
+                              bool allow_transpose) {
   const int k = threadIdx.x;
   const bool act = k < K;
   int dh = 0, dw = 0;
@@ -90,7 +93,7 @@ __device__ void build_program(Prog* pg, const T* __restrict__ wgt, float theta, 
   }
   const int hmin = wave_min_i(act ? dh : 1 << 20), hmax = wave_max_i(act ? dh : -(1 << 20));
   const int wmin = wave_min_i(act ? dw : 1 << 20), wmax = wave_max_i(act ? dw : -(1 << 20));
-  const bool tr = (wmax - wmin) > (hmax - hmin);
+  const bool tr = allow_transpose && (wmax - wmin) > (hmax - hmin);
   const int a = tr ? dw : dh;  // staging-frame row offset of the tap
   const int b = tr ? dh : dw;  // staging-frame column offset
 
@@ -137,21 +140,31 @@ __device__ void build_program(Prog* pg, const T* __restrict__ wgt, float theta, 
   const int nxt = later ? lobit(later) : 64;
   const int L = popc(cellm & below_mask(nxt)) - ci_st2;
   const int t = (sg > 0) ? pos2 : (L - 1 - pos2);  // position along +u
-  const int slot = ci_st2 + t;
   const bool allfin = popc(__ballot(act && !fin)) == 0;
+
+  // Runs are stored grouped by length so the kernels can run one tight loop
+  // per length: run `run` goes to slot group_start(L) + rank among runs of length L.
+  const bool is_start = cell && ((start2 >> k) & 1ull);
+  int rstart = 0, rslot = 0;
+  for (int l = 1; l <= kLmax; ++l) {
+    const uint64_t m = __ballot(is_start && L == l);
+    if (is_start && L == l) rslot = rstart + popc(m & below);
+    if (k == 0) pg->group[l - 1] = rstart;
+    rstart += popc(m);
+  }
+  if (k == 0) pg->group[kLmax] = rstart;
+  // the slot of a cell's run, read from the run's start lane
+  const int my_slot = __shfl(rslot, st2, 64);
 
   // (the index checks below never fail for a well-formed program; they keep
   // every LDS write inside its array whatever the inputs)
-  if (cell && run >= 0 && run < kMaxRuns && t >= 0 && t < 8 && L >= 1 && L <= kLmax) {
-    pg->run_w[run * 8 + t] = allfin ? cw : __builtin_nanf("");  // a non-finite angle poisons the channel
-    if (t == 0) {
-      pg->run_off[run] = a * S + b;
-      pg->run_len[run] = L;
-      pg->run_slot[run] = ci_st2;
-    }
+  if (cell && my_slot >= 0 && my_slot < kMaxRuns && t >= 0 && t < 8 && L >= 1 && L <= kLmax) {
+    pg->run_w[my_slot * 8 + t] = allfin ? cw : __builtin_nanf("");  // a non-finite angle poisons the channel
+    if (t == 0) pg->run_off[my_slot] = a * S + b;
   }
-  const int tslot = __shfl(slot, dup ? k - 1 : k, 64);
-  if (act) pg->tap_slot[k] = (tslot >= 0 && tslot < K) ? tslot : 0;
+  if (cell && ci >= 0 && ci < kMaxTaps) pg->cell_off[ci] = a * S + b;
+  const int tcell = __shfl(ci, dup ? k - 1 : k, 64);
+  if (act) pg->tap_cell[k] = (tcell >= 0 && tcell < K) ? tcell : 0;
   if (k == 0) {
     pg->nruns = popc(start2);
     pg->ncells = ncells;
@@ -159,6 +172,7 @@ __device__ void build_program(Prog* pg, const T* __restrict__ wgt, float theta, 
     pg->transposed = tr ? 1 : 0;
     pg->finite = allfin ? 1 : 0;
   }
+  (void)run;
 }
 
 // ---------------------------------------------------------------- strips
@@ -184,40 +198,37 @@ __device__ __forceinline__ Strip strip_of(int wt, int lane, int RB, int CB, int 
   return sp;
 }
 
-// One run of length L along u = (1, SD): acc[i] += w[t] * V[i + t], V[m] = p[m * (S + SD)].
+// All runs of length L along u = (1, SD): acc[i] += w[t] * V[i + t], V[m] = p[m * (S + SD)].
 template <int S, int SD, int L>
-__device__ __forceinline__ void run_body(const float* __restrict__ p, const float* __restrict__ wr, float (&acc)[kR]) {
-  constexpr int M = kR + L - 1;
-  float v[M];
+__device__ __forceinline__ void run_group(const Prog* __restrict__ pg, const float* __restrict__ base, int r0, int r1,
+                                          float (&acc)[kR]) {
+  for (int r = r0; r < r1; ++r) {
+    const float* p = base + pg->run_off[r];
+    const float4 wa = *reinterpret_cast<const float4*>(&pg->run_w[r * 8]);
+    float4 wb = wa;
+    if (L > 4) wb = *reinterpret_cast<const float4*>(&pg->run_w[r * 8 + 4]);
+    const float w[8] = {wa.x, wa.y, wa.z, wa.w, wb.x, wb.y, wb.z, wb.w};
+    constexpr int M = kR + L - 1;
+    float v[M];
 #pragma unroll
-  for (int m = 0; m < M; ++m) v[m] = p[m * (S + SD)];
-  float w[L];
+    for (int m = 0; m < M; ++m) v[m] = p[m * (S + SD)];
 #pragma unroll
-  for (int t = 0; t < L; ++t) w[t] = wr[t];
+    for (int t = 0; t < L; ++t)
 #pragma unroll
-  for (int t = 0; t < L; ++t)
-#pragma unroll
-    for (int i = 0; i < kR; ++i) acc[i] = fmaf(w[t], v[i + t], acc[i]);
+      for (int i = 0; i < kR; ++i) acc[i] = fmaf(w[t], v[i + t], acc[i]);
+  }
 }
 
 template <int S, int SD>
-__device__ __forceinline__ void strip_gather(const Prog* __restrict__ pg, const float* __restrict__ base,
-                                             float (&acc)[kR]) {
-  const int nruns = min(__builtin_amdgcn_readfirstlane(pg->nruns), kMaxRuns);
-  for (int r = 0; r < nruns; ++r) {
-    const int L = __builtin_amdgcn_readfirstlane(pg->run_len[r]);
-    const float* p = base + pg->run_off[r];
-    const float* wr = &pg->run_w[r * 8];
-    switch (L) {
-      case 1: run_body<S, SD, 1>(p, wr, acc); break;
-      case 2: run_body<S, SD, 2>(p, wr, acc); break;
-      case 3: run_body<S, SD, 3>(p, wr, acc); break;
-      case 4: run_body<S, SD, 4>(p, wr, acc); break;
-      case 5: run_body<S, SD, 5>(p, wr, acc); break;
-      case 6: run_body<S, SD, 6>(p, wr, acc); break;
-      default: run_body<S, SD, 7>(p, wr, acc); break;
-    }
-  }
+__device__ __forceinline__ void strip_gather(const Prog* __restrict__ pg, const int (&grp)[kLmax + 1],
+                                             const float* __restrict__ base, float (&acc)[kR]) {
+  run_group<S, SD, 1>(pg, base, grp[0], grp[1], acc);
+  run_group<S, SD, 2>(pg, base, grp[1], grp[2], acc);
+  run_group<S, SD, 3>(pg, base, grp[2], grp[3], acc);
+  run_group<S, SD, 4>(pg, base, grp[3], grp[4], acc);
+  run_group<S, SD, 5>(pg, base, grp[4], grp[5], acc);
+  run_group<S, SD, 6>(pg, base, grp[5], grp[6], acc);
+  run_group<S, SD, 7>(pg, base, grp[6], grp[7], acc);
 }
 
 // Channel-level geometry shared by both kernels.
@@ -278,14 +289,18 @@ __global__ __launch_bounds__(kThreads2) void gather_runs(RunsParams P, const T* 
   Prog* pg = reinterpret_cast<Prog*>(smem);
   float* tile = smem + kProgDwords;
   const int c = blockIdx.y;
-  const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
+  const int tid = threadIdx.x, lane = tid & 63;
+  const int wave = __builtin_amdgcn_readfirstlane(tid >> 6);
   const int nwaves = blockDim.x >> 6;
   const int HW = P.H * P.W;
 
   for (int i = tid; i < P.G * P.PS; i += blockDim.x) tile[i] = 0.f;  // halos and margins stay zero
-  if (wave == 0) build_program<T, S>(pg, wgt, theta[c], c, P.K, P.sign);
+  if (wave == 0) build_program<T, S>(pg, wgt, theta[c], c, P.K, P.sign, true);
   __syncthreads();
   const Frame f = frame_of(pg, P);
+  int grp[kLmax + 1];
+#pragma unroll
+  for (int l = 0; l <= kLmax; ++l) grp[l] = min(__builtin_amdgcn_readfirstlane(pg->group[l]), kMaxRuns);
   int src[kMaxStage], dst[kMaxStage], cmp[kMaxStage], gq[kMaxStage];
   staging_slots<S>(P, f, src, dst, cmp, gq);
 
@@ -322,11 +337,11 @@ __global__ __launch_bounds__(kThreads2) void gather_runs(RunsParams P, const T* 
 #pragma unroll
       for (int i = 0; i < kR; ++i) acc[i] = 0.f;
       if (f.s == 0)
-        strip_gather<S, 0>(pg, base, acc);
+        strip_gather<S, 0>(pg, grp, base, acc);
       else if (f.s > 0)
-        strip_gather<S, 1>(pg, base, acc);
+        strip_gather<S, 1>(pg, grp, base, acc);
       else
-        strip_gather<S, -1>(pg, base, acc);
+        strip_gather<S, -1>(pg, grp, base, acc);
       if (ok) {
         T* o = out + ((size_t)n * P.C + c) * HW;
 #pragma unroll
@@ -341,65 +356,42 @@ __global__ __launch_bounds__(kThreads2) void gather_runs(RunsParams P, const T* 
 
 // ---------------------------------------------------------------- weight gradient
 
-// One run: partial dot products d[t] = sum_i g[i] * V[i + t] added to the
-// lane's column of the run's cell slots.
-template <int S, int SD, int L>
-__device__ __forceinline__ void wrun_body(const float* __restrict__ p, const float (&g)[kR], float* __restrict__ acc) {
-  constexpr int M = kR + L - 1;
-  float v[M];
-#pragma unroll
-  for (int m = 0; m < M; ++m) v[m] = p[m * (S + SD)];
-#pragma unroll
-  for (int t = 0; t < L; ++t) {
-    float d = 0.f;
-#pragma unroll
-    for (int i = 0; i < kR; ++i) d = fmaf(g[i], v[i + t], d);
-    atomicAdd(&acc[t * 64], d);
-  }
-}
-
-template <int S, int SD>
-__device__ __forceinline__ void strip_wgrad(const Prog* __restrict__ pg, const float* __restrict__ base,
-                                            const float (&g)[kR], float* __restrict__ acc_lane, int K) {
-  const int nruns = min(__builtin_amdgcn_readfirstlane(pg->nruns), kMaxRuns);
-  for (int r = 0; r < nruns; ++r) {
-    const int L = __builtin_amdgcn_readfirstlane(pg->run_len[r]);
-    const int slot = __builtin_amdgcn_readfirstlane(pg->run_slot[r]);
-    if (slot < 0 || slot + L > K) continue;  // never taken for a well-formed program
-    const float* p = base + pg->run_off[r];
-    float* a = acc_lane + slot * 64;
-    switch (L) {
-      case 1: wrun_body<S, SD, 1>(p, g, a); break;
-      case 2: wrun_body<S, SD, 2>(p, g, a); break;
-      case 3: wrun_body<S, SD, 3>(p, g, a); break;
-      case 4: wrun_body<S, SD, 4>(p, g, a); break;
-      case 5: wrun_body<S, SD, 5>(p, g, a); break;
-      case 6: wrun_body<S, SD, 6>(p, g, a); break;
-      default: wrun_body<S, SD, 7>(p, g, a); break;
-    }
-  }
-}
-
-template <typename T, int S>
+// The weight gradient keeps one register accumulator per distinct cell and
+// lane (a static loop over the cells, so every accumulator index is a
+// compile-time constant), reads the staged x through each cell's offset for
+// the 7 outputs of the lane's strip and multiplies by the strip's dy.  No
+// atomics: the lanes' sums are reduced once per workgroup at the end, in a
+// fixed order, so the result is bitwise reproducible.
+template <typename T, int S, int KB>
 __global__ __launch_bounds__(kThreads2) void wgrad_runs(RunsParams P, const T* __restrict__ x, const T* __restrict__ dy,
                                                         const float* __restrict__ theta, float* __restrict__ partial) {
   extern __shared__ float smem[];
   Prog* pg = reinterpret_cast<Prog*>(smem);
   const int HW = P.H * P.W;
-  float* acc = smem + kProgDwords;   // [K slots][64 lanes]
-  float* gt = acc + P.K * 64;         // dy in the staging frame, no halo: [G][Hs][Ws]
+  float* red = smem + kProgDwords;  // [8 waves][64] per-wave cell sums
+  float* gt = red + 8 * 64;         // dy, compact: [G][H][W]
   float* tile = gt + ((P.G * HW + 3) & ~3);
   const int c = blockIdx.y;
-  const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
+  const int tid = threadIdx.x, lane = tid & 63;
+  const int wave = __builtin_amdgcn_readfirstlane(tid >> 6);
   const int nwaves = blockDim.x >> 6;
 
   for (int i = tid; i < P.G * P.PS; i += blockDim.x) tile[i] = 0.f;
-  for (int i = tid; i < P.K * 64; i += blockDim.x) acc[i] = 0.f;
-  if (wave == 0) build_program<T, S>(pg, static_cast<const T*>(nullptr), theta[c], c, P.K, 1);
+  if (wave == 0) build_program<T, S>(pg, static_cast<const T*>(nullptr), theta[c], c, P.K, 1, false);
   __syncthreads();
-  const Frame f = frame_of(pg, P);
+  Frame f = frame_of(pg, P);  // plane frame (no transpose); vertical strips
+  f.s = 0;
+  f.nj = f.Ws;
+  f.jlo = 0;
+  f.nc_tiles = (f.nj + P.CB - 1) / P.CB;
+  f.tiles = P.G * f.nb_tiles * f.nc_tiles;
+  const int ncells = min(__builtin_amdgcn_readfirstlane(pg->ncells), KB);
   int src[kMaxStage], dst[kMaxStage], cmp[kMaxStage], gq[kMaxStage];
   staging_slots<S>(P, f, src, dst, cmp, gq);
+
+  float acc[KB];
+#pragma unroll
+  for (int ci = 0; ci < KB; ++ci) acc[ci] = 0.f;
 
   const int n_begin = blockIdx.z * P.NPW;
   const int n_end = min(P.N, n_begin + P.NPW);
@@ -432,37 +424,41 @@ __global__ __launch_bounds__(kThreads2) void wgrad_runs(RunsParams P, const T* _
     if (n0 + P.G < n_end) load_group(n0 + P.G);
 
     for (int wt = wave; wt < f.tiles; wt += nwaves) {
-      const Strip sp = strip_of(wt, lane, P.RB, P.CB, f.nb_tiles, f.nc_tiles, f.jlo);
+      const Strip sp = strip_of(wt, lane, P.RB, P.CB, f.nb_tiles, f.nc_tiles, 0);
       const int n = n0 + sp.g;
-      const bool ok = sp.band < f.nb && sp.j - f.jlo < f.nj && n < n_end;
+      const bool ok = sp.band < f.nb && sp.j < f.Ws && n < n_end;
       const int b0 = sp.band * kR;
       const float* base = tile + (ok ? sp.g * P.PS + (b0 + P.RT) * S + sp.j : P.RT * S);
       float g[kR];
 #pragma unroll
       for (int i = 0; i < kR; ++i) {
-        const int rs = b0 + i, cs = sp.j + f.s * i;
-        g[i] = (ok && rs < f.Hs && cs >= 0 && cs < f.Ws) ? gt[sp.g * HW + rs * f.Ws + cs] : 0.f;
+        const int rs = b0 + i;
+        g[i] = (ok && rs < f.Hs) ? gt[sp.g * HW + rs * f.Ws + sp.j] : 0.f;
       }
-      if (f.s == 0)
-        strip_wgrad<S, 0>(pg, base, g, acc + lane, P.K);
-      else if (f.s > 0)
-        strip_wgrad<S, 1>(pg, base, g, acc + lane, P.K);
-      else
-        strip_wgrad<S, -1>(pg, base, g, acc + lane, P.K);
+#pragma unroll
+      for (int ci = 0; ci < KB; ++ci) {
+        if (ci >= ncells) break;
+        const float* p = base + pg->cell_off[ci];
+#pragma unroll
+        for (int i = 0; i < kR; ++i) acc[ci] = fmaf(g[i], p[i * S], acc[ci]);
+      }
     }
   }
-  __syncthreads();
-  const int ncells = min(pg->ncells, P.K);
-  for (int sl = wave; sl < ncells; sl += nwaves) {
-    float v = acc[sl * 64 + lane];
+  // lane sums -> per-wave sums -> per-tap partial of this workgroup, fixed order
+#pragma unroll
+  for (int ci = 0; ci < KB; ++ci) {
+    if (ci >= ncells) break;
+    float v = acc[ci];
 #pragma unroll
     for (int m = 32; m >= 1; m >>= 1) v += __shfl_xor(v, m, 64);
-    if (lane == 0) acc[sl * 64] = v;
+    if (lane == 0) red[wave * 64 + ci] = v;
   }
   __syncthreads();
   const size_t part = blockIdx.z;
   for (int k = tid; k < P.K; k += blockDim.x) {
-    const float v = acc[pg->tap_slot[k] * 64];
+    const int ci = min(pg->tap_cell[k], KB - 1);
+    float v = 0.f;
+    for (int w = 0; w < nwaves; ++w) v += red[w * 64 + ci];
     partial[(part * P.C + c) * (size_t)P.K + k] = pg->finite ? v : __builtin_nanf("");
   }
 }
@@ -496,14 +492,21 @@ hipError_t gather_s(const RunsPlan& pl, const void* in, const void* w, const flo
   return hipGetLastError();
 }
 
+template <typename T, int S, int KB>
+hipError_t wgrad_launch(const RunsPlan& pl, const void* x, const void* dy, const float* theta, float* partial,
+                        hipStream_t stream) {
+  hipError_t e = lds_attr(wgrad_runs<T, S, KB>);
+  if (e != hipSuccess) return e;
+  hipLaunchKernelGGL((wgrad_runs<T, S, KB>), dim3(1, (unsigned)pl.p.C, (unsigned)pl.blocks_n), dim3(pl.threads),
+                     pl.lds_bytes, stream, pl.p, static_cast<const T*>(x), static_cast<const T*>(dy), theta, partial);
+  return hipGetLastError();
+}
+
 template <typename T, int S>
 hipError_t wgrad_s(const RunsPlan& pl, const void* x, const void* dy, const float* theta, void* dw, float* partial,
                    hipStream_t stream) {
-  hipError_t e = lds_attr(wgrad_runs<T, S>);
-  if (e != hipSuccess) return e;
-  hipLaunchKernelGGL((wgrad_runs<T, S>), dim3(1, (unsigned)pl.p.C, (unsigned)pl.blocks_n), dim3(pl.threads),
-                     pl.lds_bytes, stream, pl.p, static_cast<const T*>(x), static_cast<const T*>(dy), theta, partial);
-  e = hipGetLastError();
+  hipError_t e = pl.p.K <= 32 ? wgrad_launch<T, S, 32>(pl, x, dy, theta, partial, stream)
+                              : wgrad_launch<T, S, 64>(pl, x, dy, theta, partial, stream);
   if (e != hipSuccess) return e;
   const int CK = pl.p.C * pl.p.K;
   hipLaunchKernelGGL(wgrad_reduce<T>, dim3((unsigned)((CK + 255) / 256)), dim3(256), 0, stream, partial,
