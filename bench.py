@@ -55,7 +55,9 @@ def parse():
     ap.add_argument("--no-cpu", action="store_true", help="skip the CPU oracle baseline")
     ap.add_argument("--cpu-seconds", type=float, default=12.0, help="target CPU work for the oracle sample")
     ap.add_argument("--angle-sweep", action="store_true", help="time every K of the angle-cost sweep")
-    ap.add_argument("--only", default="", help="profiling aid: run only this op (fwd|bwd_input|bwd_weight)")
+    ap.add_argument("--only", default="", help="profiling aid: run only this op (fwd|bwd_input|bwd_weight), or "
+                    "'copy': a plain elementwise copy of one N*C*H*W tensor (reads T bytes, writes T bytes), "
+                    "the calibration kernel for the HBM byte counters")
     return ap.parse_args()
 
 
@@ -74,6 +76,11 @@ class BufferSet:
 
 
 def run_ops(ops, b, K, only=""):
+    if only == "copy":
+        # torch's vectorised elementwise kernel: reads x once, writes y once
+        import torch
+        torch.neg(b.x, out=b.y)
+        return
     if not only or only == "fwd":
         ops.fwd(b.x, b.w, b.th, out=b.y)
     if not only or only == "bwd_input":
@@ -126,7 +133,7 @@ def cpu_baseline(wl, synth, seconds):
     x, dy, w = (np.asarray(d[k], np.float64) for k in ("x", "dy", "w"))
     th = np.asarray(d["theta"], np.float64)
     reps, t_total = 0, 0.0
-    while t_total < seconds and reps < 50:
+    while t_total < seconds:
         t0 = time.perf_counter()
         oracle.fwd(x, w, th, threads)
         oracle.bwd_input(dy, w, th, threads)
@@ -178,7 +185,7 @@ def main():
     ms, durs = time_workload(wl, args.steps, args.warmup, args.sets, torch, ops, synth, args.only)
     print(f"[bench] {ms:.4f} ms/step", file=sys.stderr, flush=True)
 
-    op_bytes = {"fwd": 2 * T, "bwd_input": 2 * T, "bwd_weight": 2 * T + wl.C * wl.K * wl.elem_bytes}
+    op_bytes = {"fwd": 2 * T, "bwd_input": 2 * T, "bwd_weight": 2 * T + wl.C * wl.K * wl.elem_bytes, "copy": 2 * T}
     per_op = {}
     for nm, v in durs.items():
         mean = statistics.fmean(v)

@@ -25,8 +25,8 @@
 //
 // The forward pass and the input gradient share the gather kernel (the
 // gradient gathers dy through the negated cells).  The weight gradient walks
-// the same strips and runs with the roles of data and weights exchanged and
-// accumulates per-cell partial sums in LDS.
+// the plane's own strips, keeps one register partial sum per distinct cell
+// and reduces them in a fixed order (no atomics).
 #include <hip/hip_runtime.h>
 #include <stdint.h>
 
