@@ -10,7 +10,7 @@
 #include "o1d.h"
 #include "o1d_launch.h"
 #include "o1d_plan.h"
-#include "o1d_runs.h"
+#include "o1d_line.h"
 
 namespace {
 
@@ -52,22 +52,34 @@ o1d_status_t check_sizes(const char* fn, int N, int C, int H, int W, int K, o1d_
   return O1D_OK;
 }
 
-// Kernel family: the run-decomposed kernels cover K <= 63 and planes that fit
-// in LDS with their halo; everything else takes the general tiled kernels.
-// O1D_KERNEL=tiled forces the tiled kernels (a comparison aid).
-bool runs_allowed() {
+// Kernel family: the line kernels cover K <= 63, planes up to 64 columns and
+// haloed tiles that fit in LDS; everything else takes the general tiled
+// kernels.  O1D_KERNEL=tiled forces the tiled kernels (a comparison aid).
+bool line_allowed() {
   const char* e = getenv("O1D_KERNEL");
   return !(e && e[0] == 't');
 }
 
-o1d::runs::RunsPlan runs_plan(int N, int C, int H, int W, int K, int sign, int kind) {
-  if (!runs_allowed()) return o1d::runs::RunsPlan();
-  return o1d::runs::plan_runs(N, C, H, W, K, sign, kind);
+o1d::line::LinePlan line_plan(int N, int C, int H, int W, int K, int sign, int kind, bool vec_ok) {
+  if (!line_allowed()) return o1d::line::LinePlan();
+  return o1d::line::plan_line(N, C, H, W, K, sign, kind, vec_ok);
 }
 
+// Vector staging needs 16-byte (float32) or 8-byte (bfloat16) aligned tensors.
+bool vec_aligned(const void* p, o1d_dtype_t dt) { return ((uintptr_t)p % (dt == O1D_BF16 ? 8u : 16u)) == 0; }
+
+// The workspace size must not depend on pointer alignment: take the larger
+// partial count of the two staging variants.
 size_t wgrad_workspace(int N, int C, int H, int W, int K) {
-  const o1d::runs::RunsPlan rp = runs_plan(N, C, H, W, K, 1, 1);
-  const size_t parts = rp.ok ? (size_t)rp.blocks_n : o1d::plan_wgrad(N, C, H, W, K).parts();
+  const o1d::line::LinePlan a = line_plan(N, C, H, W, K, 1, 1, true);
+  const o1d::line::LinePlan b = line_plan(N, C, H, W, K, 1, 1, false);
+  size_t parts = 0;
+  if (a.ok || b.ok) {
+    if (a.ok) parts = (size_t)a.blocks_n;
+    if (b.ok && (size_t)b.blocks_n > parts) parts = (size_t)b.blocks_n;
+  } else {
+    parts = o1d::plan_wgrad(N, C, H, W, K).parts();
+  }
   return parts * (size_t)C * (size_t)K * sizeof(float);
 }
 
@@ -87,8 +99,8 @@ o1d_status_t gather_entry(const char* fn, const void* in, const void* w, const f
   if (overlaps(in, bytes, out, bytes)) return fail(O1D_ERR_INVALID, "%s: output overlaps input", fn);
   (void)hipGetLastError();
   hipStream_t s = static_cast<hipStream_t>(stream);
-  const o1d::runs::RunsPlan rp = runs_plan(N, C, H, W, K, sign, 0);
-  if (rp.ok) return hip_status(fn, o1d::launch_gather_runs((o1d::Dtype)dt, rp, in, w, theta, out, s));
+  const o1d::line::LinePlan lp = line_plan(N, C, H, W, K, sign, 0, vec_aligned(in, dt) && vec_aligned(out, dt));
+  if (lp.ok) return hip_status(fn, o1d::launch_gather_line((o1d::Dtype)dt, lp, in, w, theta, out, s));
   return hip_status(fn, o1d::launch_gather((o1d::Dtype)dt, in, w, theta, out, N, C, H, W, K, sign, s));
 }
 
@@ -132,9 +144,10 @@ o1d_status_t o1d_bwd_weight(const void* x, const void* dy, const float* theta_de
       (need > 0 && (overlaps(workspace, need, x, tbytes) || overlaps(workspace, need, dy, tbytes) ||
                     overlaps(workspace, need, dw, dwbytes))))
     return fail(O1D_ERR_INVALID, "%s: dw or workspace overlaps an input", fn);
-  const o1d::runs::RunsPlan rp = runs_plan(N, C, H, W, K, 1, 1);
-  if (rp.ok)
-    return hip_status(fn, o1d::launch_wgrad_runs((o1d::Dtype)dtype, rp, x, dy, theta_deg, dw,
+  const o1d::line::LinePlan lp =
+      line_plan(N, C, H, W, K, 1, 1, vec_aligned(x, dtype) && vec_aligned(dy, dtype));
+  if (lp.ok)
+    return hip_status(fn, o1d::launch_wgrad_line((o1d::Dtype)dtype, lp, x, dy, theta_deg, dw,
                                                  static_cast<float*>(workspace), s));
   return hip_status(fn, o1d::launch_wgrad((o1d::Dtype)dtype, x, dy, theta_deg, dw, static_cast<float*>(workspace), N,
                                           C, H, W, K, s));
