@@ -69,17 +69,14 @@ o1d::line::LinePlan line_plan(int N, int C, int H, int W, int K, int sign, int k
 bool vec_aligned(const void* p, o1d_dtype_t dt) { return ((uintptr_t)p % (dt == O1D_BF16 ? 8u : 16u)) == 0; }
 
 // The workspace size must not depend on pointer alignment: take the larger
-// partial count of the two staging variants.
+// partial count of the kernels that aligned and unaligned tensors select
+// (the line kernels need aligned tensors; otherwise the tiled kernels run).
 size_t wgrad_workspace(int N, int C, int H, int W, int K) {
   const o1d::line::LinePlan a = line_plan(N, C, H, W, K, 1, 1, true);
   const o1d::line::LinePlan b = line_plan(N, C, H, W, K, 1, 1, false);
-  size_t parts = 0;
-  if (a.ok || b.ok) {
-    if (a.ok) parts = (size_t)a.blocks_n;
-    if (b.ok && (size_t)b.blocks_n > parts) parts = (size_t)b.blocks_n;
-  } else {
-    parts = o1d::plan_wgrad(N, C, H, W, K).parts();
-  }
+  const size_t tiled = o1d::plan_wgrad(N, C, H, W, K).parts();
+  const size_t pa = a.ok ? (size_t)a.blocks_n : tiled, pb = b.ok ? (size_t)b.blocks_n : tiled;
+  const size_t parts = pa > pb ? pa : pb;
   return parts * (size_t)C * (size_t)K * sizeof(float);
 }
 

@@ -68,9 +68,9 @@ struct LineParams {
   int GPS;    // floats per dy slot
   int aux;    // float offset of the bounce / dy area in dynamic LDS
   int red;    // float offset of the per-wave reduction area (weight gradient)
-  int vw;     // staging: 4 = vector accesses of 4 elements, 1 = scalar
-  int ks;     // staging: row steps per plane
-  int ms;     // staging: column segments per plane
+  int trash;  // float offset of the trash area (staging writes of slots outside the plane)
+  int ks;     // staging: row steps per plane (32 rows each)
+  int ms;     // staging: column segments per plane (32 columns each)
 };
 
 struct LinePlan {
@@ -86,10 +86,12 @@ inline size_t round4(size_t v) { return (v + 3) & ~(size_t)3; }
 
 // kind: 0 = gather (forward / input gradient), 1 = weight gradient.
 // vec_ok: the tensors are aligned for vector accesses (16 bytes for float32,
-// 8 bytes for bfloat16), so that rows of a W % 4 == 0 plane can use them.
+// 8 bytes for bfloat16).  Staging moves 4 elements of a row per access, so
+// the plan needs W % 4 == 0 and aligned tensors (else the tiled kernels run).
 inline LinePlan plan_line(int N, int C, int H, int W, int K, int sign, int kind, bool vec_ok = true) {
   LinePlan pl;
   if (K < 1 || K > kMaxTaps || N < 1 || C < 1 || H < 1 || W < 1) return pl;
+  if (W % 4 != 0 || !vec_ok) return pl;
   const int M = H > W ? H : W;
   const int halo = (K / 2) < (M - 1) ? (K / 2) : (M - 1);
   // rows covered by whole bands, worst case over both frames and strip shapes
@@ -123,32 +125,21 @@ inline LinePlan plan_line(int N, int C, int H, int W, int K, int sign, int kind,
   p.GS = S;
   p.GPS = (int)round4((size_t)cover * S);
   const long long HW = (long long)H * W;
-  // staging (see o1d_line_kernels.h): vector slots of 4 elements when the
-  // rows allow it (kMaxSlots / 4 per thread), else scalar slots (kMaxSlots)
+  // staging (see o1d_line_kernels.h): kMaxSlots / 4 vector slots per thread,
+  // each a step of 32 rows and a segment of 32 columns of one plane
   if (W > 64) return pl;
-  int vw = 1, ks = 0, ms = 1, qmax = kMaxSlots;
-  if (W % 4 == 0 && vec_ok) {
-    vw = 4;
-    ks = cdiv(H, 32);
-    ms = cdiv(W, 32);
-    qmax = kMaxSlots / 4;
-  }
-  if (vw == 1 || ks * ms > qmax) {
-    vw = 1;
-    ms = 1;
-    qmax = kMaxSlots;
-    const int lw = W <= 16 ? 16 : (W <= 32 ? 32 : 64);
-    ks = cdiv(H, kWaves * (64 / lw));
-  }
-  const int gmax_slots = qmax / (ks * ms);
+  const int ks = cdiv(H, 32), ms = cdiv(W, 32);
+  const int gmax_slots = (kMaxSlots / 4) / (ks * ms);
   if (gmax_slots < 1) return pl;
-  p.vw = vw;
   p.ks = ks;
   p.ms = ms;
+  // trash area: a word per lane plus the reach of a transposed vector write
+  const int trash = (int)round4((size_t)(64 + 3 * S + 4));
   auto lds_for = [&](int g) -> size_t {
     size_t f = (size_t)kProgFloats + (size_t)g * p.PS;
     f += (size_t)g * (kind == 0 ? p.OPS : p.GPS);
     if (kind == 1) f += (size_t)kWaves * 64;
+    f += (size_t)trash;
     return f * 4;
   };
   // lane iterations per plane group, worst case over frames and strip shapes
@@ -175,10 +166,12 @@ inline LinePlan plan_line(int N, int C, int H, int W, int K, int sign, int kind,
   while (G > 1 && (lds_for(G) > kLdsBudget || iters(G) > kMaxIt)) --G;
   if (iters(G) > kMaxIt) return pl;
   if (lds_for(G) > kMaxLdsBytes) return pl;
-  if ((long long)(G + 1) * C * HW >= (1ll << 31)) return pl;
+  // buffer resources cover a group in bytes (float32 at most), below 2^31
+  if ((long long)(G + 1) * C * HW * 4 >= (1ll << 31)) return pl;
   p.G = G;
   p.aux = kProgFloats + G * p.PS;
   p.red = p.aux + G * (kind == 0 ? p.OPS : p.GPS);
+  p.trash = p.red + (kind == 1 ? kWaves * 64 : 0);
   // images per workgroup: about three resident workgroups per CU over 256 CUs
   const size_t lds = lds_for(G);
   int per_cu = (int)(kMaxLdsBytes / lds);

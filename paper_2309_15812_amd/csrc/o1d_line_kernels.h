@@ -76,10 +76,7 @@ struct Prog {
   int tr;      // staging frame = transposed plane
   int s;       // strip step u = (1, s) in the staging frame
   int finite;  // the channel's angle is finite
-  int vw;      // staging: elements per lane slot
-  int ks;      // staging: row steps per plane
-  int ms;      // staging: column segments per plane
-  int pad_[9];
+  int pad_[12];
   uint32_t contm[2];  // bit c: cell c is cell c - 1 moved by u
   int pad2_[30];
   int16_t off[64];    // LDS offset of every cell from the output pixel, cell order (rows increasing)
@@ -609,186 +606,142 @@ __device__ __forceinline__ Task task_at(const LineParams& P, const Frame& f, con
   return k;
 }
 
-// Staging of one plane group through registers.  Two lane layouts:
-//  * vector (vw = 4, W % 4 == 0, 16-byte aligned tensors): every lane moves
-//    4 consecutive elements with one 16-byte (bf16: 8-byte) global access.
-//    A half-wave covers 4 rows x 8 quads: lane -> row (lane >> 3) & 3 (+4 in
-//    the second half-wave, +8 per wave), quad lane & 7.  For an odd LDS row
-//    stride the 32 component writes of a half-wave then hit 32 distinct
-//    banks in either frame.  Steps of 32 rows and segments of 32 columns.
-//  * scalar (vw = 1): lane -> column lane % LW (LW = 16, 32 or 64 >= W),
-//    row lane / LW (+ 64 / LW per wave); steps of 4 * 64 / LW rows.
-// Slot q = (g, k, m): plane g of the group, row step k, column segment m,
-// m fastest.  Every per-slot offset is a per-lane base plus a wave-uniform
-// increment.
-struct Stage {
-  int vw;          // elements per lane slot: 4 or 1
-  int rs, ks;      // rows per step, steps per plane
-  int cs, ms;      // columns per segment, segments per plane
-  int nq;          // slots per plane group (G * ks * ms)
-  int hr, w0;      // this lane's first row and column
-  int src0;        // element offset of (hr, w0) in a plane
-  bool lane_ok;    // w0 < W
-};
+// Staging of one plane group through registers.  Every lane moves 4
+// consecutive elements of a plane row per slot with one 16-byte (bf16:
+// 8-byte) buffer access.  A half-wave covers 4 rows x 8 quads: lane -> row
+// (lane >> 3) & 3 (+4 in the second half-wave, +8 per wave), quad lane & 7.
+// For an odd LDS row stride the 32 component writes of a half-wave then hit
+// 32 distinct banks in either frame.  Slot q = (g, k, m): plane g of the
+// group, row step k (32 rows), column segment m (32 columns), m fastest.
+//
+// A lane's slot addresses are computed once per workgroup:
+//  * goff[q]: byte offset of its 4 elements from the group's first element,
+//    or kOob for a slot outside the plane.  Buffer accesses beyond the
+//    resource's size read zeros and drop stores, and a group's resource
+//    covers only its ng planes, so absent slots and planes need no branch.
+//  * LDS addresses of the first element in a tile, or of the lane's word
+//    in the trash area (written, never read) for a slot outside the plane.
+constexpr uint32_t kOob = 0x80000000u;
+constexpr int kQ = kMaxSlots / 4;  // vector slots per lane
 
-__host__ __device__ inline int stage_lw(int W) { return W <= 16 ? 16 : (W <= 32 ? 32 : 64); }
-
-__device__ __forceinline__ Stage make_stage(const LineParams& P, int vw, int ks, int ms) {
-  Stage st;
-  st.vw = vw;
+// Calls f(q, ok, g, h, w) for every slot: plane g of the group, plane row h
+// and first column w of the lane's 4 elements, ok = they lie in the plane.
+template <class F>
+__device__ __forceinline__ void for_each_slot(const LineParams& P, F&& f) {
   const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6;
-  if (st.vw == 4) {
-    st.rs = 32;
-    st.cs = 32;
-    st.hr = wave * 8 + (lane >> 5) * 4 + ((lane >> 3) & 3);
-    st.w0 = 4 * (lane & 7);
-  } else {
-    const int lw = stage_lw(P.W), rpw = 64 / lw;
-    st.rs = kWaves * rpw;
-    st.cs = 64;
-    st.hr = wave * rpw + lane / lw;
-    st.w0 = lane & (lw - 1);
-  }
-  st.ks = ks;
-  st.ms = ms;
-  st.nq = P.G * ks * ms;
-  st.lane_ok = st.w0 < P.W;
-  st.src0 = st.hr * P.W + st.w0;
-  return st;
-}
-
-// Walks the slots: f(q, g, h0, w0u, ok) with q the slot index (compile time),
-// g the plane, h0 = k * rs and w0u = m * cs the wave-uniform row and column
-// offsets, ok = the lane's element(s) lie in the plane and g < ng.
-template <int NQ, class F>
-__device__ __forceinline__ void for_slots(const LineParams& P, const Stage& st, int ng, F&& f) {
-  int g = 0, k = 0, m = 0;
-  static_for<NQ>([&](auto qc) __attribute__((always_inline)) {
+  const int hr = wave * 8 + (lane >> 5) * 4 + ((lane >> 3) & 3);
+  const int w0 = 4 * (lane & 7);
+  const int per = P.ks * P.ms;
+  static_for<kQ>([&](auto qc) __attribute__((always_inline)) {
     constexpr int q = decltype(qc)::value;
-    const bool ok = q < st.nq && g < ng && st.lane_ok && st.hr + k * st.rs < P.H && st.w0 + m * st.cs < P.W;
-    f(qc, g, k * st.rs, m * st.cs, ok);
-    if (++m == st.ms) {
-      m = 0;
-      if (++k == st.ks) {
-        k = 0;
-        ++g;
-      }
-    }
+    const int g = q / per, r = q - g * per, k = r / P.ms, m = r - k * P.ms;
+    const int h = hr + 32 * k, w = w0 + 32 * m;
+    f(q, g < P.G && h < P.H && w < P.W, g, h, w);
   });
 }
 
+template <typename T>
+__device__ __forceinline__ void slot_offsets(const LineParams& P, uint32_t (&goff)[kQ]) {
+  const int img = P.C * P.H * P.W;
+  for_each_slot(P, [&](int q, bool ok, int g, int h, int w) __attribute__((always_inline)) {
+    goff[q] = ok ? (uint32_t)((g * img + h * P.W + w) * (int)sizeof(T)) : kOob;
+  });
+}
+
+// Element (r, c) of tile slot g (frame coordinates: (h, w), or (w, h) when
+// transposed) is the float at byte address base + 4 * (g * pitch + r * S + c).
+template <int S>
+__device__ __forceinline__ void slot_lds(const LineParams& P, uint32_t base, int pitch, bool tr, uint32_t trash,
+                                         uint32_t (&a)[kQ]) {
+  const uint32_t tl = trash + 4 * (threadIdx.x & 63);
+  for_each_slot(P, [&](int q, bool ok, int g, int h, int w) __attribute__((always_inline)) {
+    a[q] = ok ? base + 4 * (uint32_t)(g * pitch + (tr ? w * S + h : h * S + w)) : tl;
+  });
+}
+
+// A buffer resource over `bytes` bytes from p (raw, no swizzle).
+__device__ __forceinline__ __amdgpu_buffer_rsrc_t buffer_of(const void* p, int bytes) {
+  return __builtin_amdgcn_make_buffer_rsrc(const_cast<void*>(p), (short)0, bytes, 0x00020000);
+}
+
+__device__ __forceinline__ float lds_load(uint32_t a) {
+  return *(const __attribute__((address_space(3))) float*)(uintptr_t)a;
+}
+__device__ __forceinline__ void lds_store(uint32_t a, float v) {
+  *(__attribute__((address_space(3))) float*)(uintptr_t)a = v;
+}
+
 // Raw staging registers: the loaded words are not touched until they are
-// written to LDS (converting or masking them at load time would make the
-// compiler wait for every load right after issuing it).  float32: one word
-// per element; bfloat16: vector slots keep 4 elements in 2 words, scalar
-// slots one element per word.
+// written to LDS (converting them at load time would make the compiler wait
+// for every load right after issuing it).  float32: one word per element;
+// bfloat16: 4 elements in 2 words.
 template <typename T>
 struct Raw;
 template <>
 struct Raw<float> {
-  static __device__ __forceinline__ void load4(const float* p, uint32_t* r) {
-    const uint4 v = *reinterpret_cast<const uint4*>(p);
-    r[0] = v.x; r[1] = v.y; r[2] = v.z; r[3] = v.w;
+  static constexpr int kWords = 4;
+  static __device__ __forceinline__ void load(__amdgpu_buffer_rsrc_t rs, uint32_t off, uint32_t* r) {
+    const auto v = __builtin_amdgcn_raw_buffer_load_b128(rs, off, 0, 0);
+    r[0] = v[0]; r[1] = v[1]; r[2] = v[2]; r[3] = v[3];
   }
-  static __device__ __forceinline__ float elem4(const uint32_t* r, int j) { return __uint_as_float(r[j]); }
-  static __device__ __forceinline__ uint32_t load1(const float* p) { return __float_as_uint(*p); }
-  static __device__ __forceinline__ float elem1(uint32_t r) { return __uint_as_float(r); }
+  static __device__ __forceinline__ float elem(const uint32_t* r, int j) { return __uint_as_float(r[j]); }
+  static __device__ __forceinline__ void store(__amdgpu_buffer_rsrc_t rs, uint32_t off, const float (&e)[4]) {
+    typedef unsigned int u4 __attribute__((ext_vector_type(4)));
+    u4 v;
+    v[0] = __float_as_uint(e[0]); v[1] = __float_as_uint(e[1]); v[2] = __float_as_uint(e[2]); v[3] = __float_as_uint(e[3]);
+    __builtin_amdgcn_raw_buffer_store_b128(v, rs, off, 0, 0);
+  }
 };
 template <>
 struct Raw<uint16_t> {
-  static __device__ __forceinline__ void load4(const uint16_t* p, uint32_t* r) {
-    const uint2 v = *reinterpret_cast<const uint2*>(p);
-    r[0] = v.x; r[1] = v.y;
+  static constexpr int kWords = 2;
+  static __device__ __forceinline__ void load(__amdgpu_buffer_rsrc_t rs, uint32_t off, uint32_t* r) {
+    const auto v = __builtin_amdgcn_raw_buffer_load_b64(rs, off, 0, 0);
+    r[0] = v[0]; r[1] = v[1];
   }
-  static __device__ __forceinline__ float elem4(const uint32_t* r, int j) {
+  static __device__ __forceinline__ float elem(const uint32_t* r, int j) {
     const uint32_t w = r[j >> 1];
     return __uint_as_float((j & 1) ? (w & 0xffff0000u) : (w << 16));
   }
-  static __device__ __forceinline__ uint32_t load1(const uint16_t* p) { return *p; }
-  static __device__ __forceinline__ float elem1(uint32_t r) { return __uint_as_float(r << 16); }
+  static __device__ __forceinline__ void store(__amdgpu_buffer_rsrc_t rs, uint32_t off, const float (&e)[4]) {
+    typedef unsigned int u2 __attribute__((ext_vector_type(2)));
+    u2 v;
+    v[0] = (uint32_t)from_f32<uint16_t>(e[0]) | ((uint32_t)from_f32<uint16_t>(e[1]) << 16);
+    v[1] = (uint32_t)from_f32<uint16_t>(e[2]) | ((uint32_t)from_f32<uint16_t>(e[3]) << 16);
+    __builtin_amdgcn_raw_buffer_store_b64(v, rs, off, 0, 0);
+  }
 };
 
-// Loads the slot values of planes [0, ng) of a group whose first plane
-// starts at `src` into raw registers; an unused slot reads the group's first
-// element (its value is never stored).
+// Loads the slots of a group (ng >= 1 planes from `src`) into raw registers.
 template <typename T>
-__device__ __forceinline__ void stage_load(const LineParams& P, const Stage& st, const T* __restrict__ src, int ng,
+__device__ __forceinline__ void stage_load(const LineParams& P, const T* src, int ng, const uint32_t (&goff)[kQ],
                                            uint32_t (&v)[kMaxSlots]) {
-  const int img = P.C * P.H * P.W;  // < 2^31 (checked by the plan)
-  if (st.vw == 4) {
-    constexpr int WPS = sizeof(T);  // raw words per vector slot: 4 (float32) or 2 (bfloat16)
-    for_slots<kMaxSlots / 4>(P, st, ng, [&](auto qc, int g, int h0, int w0u, bool ok) __attribute__((always_inline)) {
-      constexpr int q = decltype(qc)::value;
-      const int off = ok ? g * img + h0 * P.W + w0u + st.src0 : 0;
-      Raw<T>::load4(src + off, &v[WPS * q]);
-    });
-    // define the words bfloat16 vector slots leave unused, so that both
-    // branches end with stores to the same registers (otherwise the compiler
-    // merges the branches' last stores through a pointer select and keeps
-    // the array in scratch memory)
-#pragma unroll
-    for (int i = WPS * (kMaxSlots / 4); i < kMaxSlots; ++i) v[i] = 0u;
-  } else {
-    for_slots<kMaxSlots>(P, st, ng, [&](auto qc, int g, int h0, int w0u, bool ok) __attribute__((always_inline)) {
-      constexpr int q = decltype(qc)::value;
-      const int off = ok ? g * img + h0 * P.W + w0u + st.src0 : 0;
-      v[q] = Raw<T>::load1(src + off);
-    });
-  }
+  const __amdgpu_buffer_rsrc_t rs = buffer_of(src, ng * P.C * P.H * P.W * (int)sizeof(T));
+  static_for<kQ>([&](auto qc) __attribute__((always_inline)) {
+    constexpr int q = decltype(qc)::value;
+    Raw<T>::load(rs, goff[q], &v[Raw<T>::kWords * q]);
+  });
 }
 
-template <typename T>
-struct Vec4;
-template <>
-struct Vec4<float> {
-  typedef float4 type;
-  static __device__ __forceinline__ float4 from_f32x4(const float* i) { return make_float4(i[0], i[1], i[2], i[3]); }
-};
-template <>
-struct Vec4<uint16_t> {
-  typedef ushort4 type;
-  static __device__ __forceinline__ ushort4 from_f32x4(const float* i) {
-    return make_ushort4(from_f32<uint16_t>(i[0]), from_f32<uint16_t>(i[1]), from_f32<uint16_t>(i[2]),
-                        from_f32<uint16_t>(i[3]));
-  }
-};
-
-// Writes the slot values into a tile in the staging frame: element (h, w)
-// of plane slot g goes to base + g * pstride + (frame row) * stride + (frame
-// column), frame = (h, w), or (w, h) when transposed.  `base` points at the
-// tile position of frame (0, 0).  STRIDE > 0 is a compile-time row stride,
-// STRIDE == 0 takes `stride` at run time.
-template <typename T, int STRIDE>
-__device__ __forceinline__ void stage_store(const LineParams& P, const Stage& st, float* base, int pstride, int stride_rt,
-                                            bool tr, const uint32_t (&v)[kMaxSlots]) {
-  const int stride = STRIDE > 0 ? STRIDE : stride_rt;
-  const int r0 = tr ? st.w0 : st.hr, c0 = tr ? st.hr : st.w0;
-  float* lb = base + r0 * stride + c0;
-  if (st.vw == 4) {
-    constexpr int WPS = sizeof(T);
-    for_slots<kMaxSlots / 4>(P, st, P.G, [&](auto qc, int g, int h0, int w0u, bool ok) __attribute__((always_inline)) {
+// Writes the slots into a tile: the 4 elements of a slot are consecutive
+// along the frame's rows, or along its columns (stride S) when transposed.
+template <typename T, int S>
+__device__ __forceinline__ void stage_store(const uint32_t (&a)[kQ], bool tr, const uint32_t (&v)[kMaxSlots]) {
+  if (tr) {
+    static_for<kQ>([&](auto qc) __attribute__((always_inline)) {
       constexpr int q = decltype(qc)::value;
-      if (ok) {
-        if (tr) {
-          float* p = lb + (g * pstride + w0u * stride + h0);
-          static_for<4>([&](auto jc) __attribute__((always_inline)) {
-            p[decltype(jc)::value * stride] = Raw<T>::elem4(&v[WPS * q], decltype(jc)::value);
-          });
-        } else {
-          float* p = lb + (g * pstride + h0 * stride + w0u);
-          static_for<4>([&](auto jc) __attribute__((always_inline)) {
-            p[decltype(jc)::value] = Raw<T>::elem4(&v[WPS * q], decltype(jc)::value);
-          });
-        }
-      }
+      static_for<4>([&](auto jc) __attribute__((always_inline)) {
+        constexpr int j = decltype(jc)::value;
+        lds_store(a[q] + j * S * 4, Raw<T>::elem(&v[Raw<T>::kWords * q], j));
+      });
     });
   } else {
-    for_slots<kMaxSlots>(P, st, P.G, [&](auto qc, int g, int h0, int w0u, bool ok) __attribute__((always_inline)) {
+    static_for<kQ>([&](auto qc) __attribute__((always_inline)) {
       constexpr int q = decltype(qc)::value;
-      if (ok) {
-        float* p = lb + (tr ? g * pstride + w0u * stride + h0 : g * pstride + h0 * stride + w0u);
-        *p = Raw<T>::elem1(v[q]);
-      }
+      static_for<4>([&](auto jc) __attribute__((always_inline)) {
+        constexpr int j = decltype(jc)::value;
+        lds_store(a[q] + j * 4, Raw<T>::elem(&v[Raw<T>::kWords * q], j));
+      });
     });
   }
 }
@@ -846,24 +799,24 @@ __device__ __forceinline__ void gather_group(const LineParams& P, const Frame& f
 
 // Output bounce tile (plane orientation, row stride OS) -> global, planes
 // [0, ng) of the group at `dst`, with the staging lane layout.
+// Stores a group's outputs from the bounce tile (plane orientation, row
+// stride S) as coalesced rows.
 template <typename T>
-__device__ __forceinline__ void flush_bounce(const LineParams& P, const Stage& st, const float* otiles,
-                                             T* __restrict__ dst, int ng) {
-  const int img = P.C * P.H * P.W;
-  const float* lb = otiles + st.hr * P.OS + st.w0;
-  if (st.vw == 4) {
-    for_slots<kMaxSlots / 4>(P, st, ng, [&](auto, int g, int h0, int w0u, bool ok) __attribute__((always_inline)) {
-      if (ok) {
-        const float* p = lb + (g * P.OPS + h0 * P.OS + w0u);
-        const float e[4] = {p[0], p[1], p[2], p[3]};
-        *reinterpret_cast<typename Vec4<T>::type*>(dst + (g * img + h0 * P.W + w0u + st.src0)) = Vec4<T>::from_f32x4(e);
-      }
+__device__ __forceinline__ void flush_bounce(const LineParams& P, T* dst, int ng, const uint32_t (&lb)[kQ],
+                                             const uint32_t (&goff)[kQ]) {
+  const __amdgpu_buffer_rsrc_t rs = buffer_of(dst, ng * P.C * P.H * P.W * (int)sizeof(T));
+  float e[kQ][4];  // all reads first, so that their latencies overlap
+  static_for<kQ>([&](auto qc) __attribute__((always_inline)) {
+    constexpr int q = decltype(qc)::value;
+    static_for<4>([&](auto jc) __attribute__((always_inline)) {
+      constexpr int j = decltype(jc)::value;
+      e[q][j] = lds_load(lb[q] + 4 * j);
     });
-  } else {
-    for_slots<kMaxSlots>(P, st, ng, [&](auto, int g, int h0, int w0u, bool ok) __attribute__((always_inline)) {
-      if (ok) dst[g * img + h0 * P.W + w0u + st.src0] = from_f32<T>(lb[g * P.OPS + h0 * P.OS + w0u]);
-    });
-  }
+  });
+  static_for<kQ>([&](auto qc) __attribute__((always_inline)) {
+    constexpr int q = decltype(qc)::value;
+    Raw<T>::store(rs, goff[q], e[q]);
+  });
 }
 
 template <typename T, int S, int KB>
@@ -884,23 +837,22 @@ __global__ __launch_bounds__(kThreads) void line_gather(LineParams P, const T* _
   const T* inc = in + (size_t)c * HW;
   T* outc = out + (size_t)c * HW;
 
-  if (tid == 0) {
-    pg->vw = P.vw;
-    pg->ks = P.ks;
-    pg->ms = P.ms;
-  }
   // The first two groups' loads do not depend on the frame: issue them before
   // the program is built.  Two register buffers alternate, so every group's
   // loads are in flight for two groups' worth of compute.
+  uint32_t goff[kQ];
+  slot_offsets<T>(P, goff);
   uint32_t pa[kMaxSlots], pb[kMaxSlots];
-  {
-    const Stage st0 = make_stage(P, P.vw, P.ks, P.ms);
-    stage_load(P, st0, inc + (size_t)n_begin * img, min(P.G, n_end - n_begin), pa);
-    stage_load(P, st0, inc + (size_t)(n_begin + P.G) * img, max(0, min(P.G, n_end - n_begin - P.G)), pb);
-  }
+  stage_load(P, inc + (size_t)n_begin * img, min(P.G, n_end - n_begin), goff, pa);
+  if (n_begin + P.G < n_end)  // a second group exists (its first image is in the tensor)
+    stage_load(P, inc + (size_t)(n_begin + P.G) * img, min(P.G, n_end - n_begin - P.G), goff, pb);
   for (int i = tid; i < P.G * P.PS; i += kThreads) tiles[i] = 0.f;  // halos and guards stay zero
   if (wave == 0) build_program<T>(pg, wgt, theta[c], c, P.K, P.sign, P.H, P.W, S);
   __syncthreads();
+  const bool tr = opaque(&pg->tr) != 0;
+  uint32_t lt[kQ], lb[kQ];  // the slots in the tile (staging frame) and in the bounce tile (plane)
+  slot_lds<S>(P, lds_addr(tiles + kGuard + P.halo * S + P.halo), P.PS, tr, lds_addr(smem + P.trash), lt);
+  slot_lds<S>(P, lds_addr(otiles), P.OPS, false, lds_addr(smem + P.trash), lb);
   float wt[KB];  // the cells' weights, wave-uniform, for the whole workgroup
 #pragma unroll
   for (int i = 0; i < KB; ++i) wt[i] = pg->w[i];
@@ -909,13 +861,12 @@ __global__ __launch_bounds__(kThreads) void line_gather(LineParams P, const T* _
   auto step = [&](uint32_t (&pre)[kMaxSlots], int n0) __attribute__((always_inline)) {
     const int ng = min(P.G, n_end - n0);
     const Frame f = frame_of(pg, P);
-    const Stage st = make_stage(P, opaque(&pg->vw), opaque(&pg->ks), opaque(&pg->ms));
     __syncthreads();  // the tile and the bounce tile are free
-    stage_store<T, S>(P, st, tiles + kGuard + P.halo * S + P.halo, P.PS, 0, f.tr != 0, pre);
-    if (prev >= 0) flush_bounce<T>(P, st, otiles, outc + (size_t)prev * img, min(P.G, n_end - prev));
+    stage_store<T, S>(lt, tr, pre);
+    if (prev >= 0) flush_bounce<T>(P, outc + (size_t)prev * img, min(P.G, n_end - prev), lb, goff);
     __syncthreads();  // the group is staged
     if (n0 + 2 * P.G < n_end)
-      stage_load(P, st, inc + (size_t)(n0 + 2 * P.G) * img, min(P.G, n_end - n0 - 2 * P.G), pre);
+      stage_load(P, inc + (size_t)(n0 + 2 * P.G) * img, min(P.G, n_end - n0 - 2 * P.G), goff, pre);
     T* outn = outc + (size_t)n0 * img;
     if (f.s == 0)
       gather_group<T, S, kRv, 0, KB>(P, f, task_map(P, f, lane), wave, tiles, otiles, outn, ng, pg, wt);
@@ -930,9 +881,8 @@ __global__ __launch_bounds__(kThreads) void line_gather(LineParams P, const T* _
     if (n0 + P.G < n_end) step(pb, n0 + P.G);
   }
   if (prev >= 0) {
-    const Stage st = make_stage(P, opaque(&pg->vw), opaque(&pg->ks), opaque(&pg->ms));
     __syncthreads();
-    flush_bounce<T>(P, st, otiles, outc + (size_t)prev * img, min(P.G, n_end - prev));
+    flush_bounce<T>(P, outc + (size_t)prev * img, min(P.G, n_end - prev), lb, goff);
   }
 }
 
@@ -980,21 +930,19 @@ __global__ __launch_bounds__(kThreads) void line_wgrad(LineParams P, const T* __
   const T* xc = x + (size_t)c * HW;
   const T* dc = dy + (size_t)c * HW;
 
-  if (tid == 0) {
-    pg->vw = P.vw;
-    pg->ks = P.ks;
-    pg->ms = P.ms;
-  }
+  uint32_t goff[kQ];
+  slot_offsets<T>(P, goff);
   uint32_t px[kMaxSlots], pd[kMaxSlots];
-  {
-    const Stage st0 = make_stage(P, P.vw, P.ks, P.ms);
-    stage_load(P, st0, xc + (size_t)n_begin * img, min(P.G, n_end - n_begin), px);
-    stage_load(P, st0, dc + (size_t)n_begin * img, min(P.G, n_end - n_begin), pd);
-  }
+  stage_load(P, xc + (size_t)n_begin * img, min(P.G, n_end - n_begin), goff, px);
+  stage_load(P, dc + (size_t)n_begin * img, min(P.G, n_end - n_begin), goff, pd);
   for (int i = tid; i < P.G * P.PS; i += kThreads) tiles[i] = 0.f;
   for (int i = tid; i < P.G * P.GPS; i += kThreads) gtiles[i] = 0.f;
   if (wave == 0) build_program<T>(pg, static_cast<const T*>(nullptr), theta[c], c, P.K, 1, P.H, P.W, S);
   __syncthreads();
+  const bool tr = opaque(&pg->tr) != 0;
+  uint32_t lx[kQ], ld[kQ];  // the slots in the x tile and in the dy tile (both in the staging frame)
+  slot_lds<S>(P, lds_addr(tiles + kGuard + P.halo * S + P.halo), P.PS, tr, lds_addr(smem + P.trash), lx);
+  slot_lds<S>(P, lds_addr(gtiles + 6), P.GPS, tr, lds_addr(smem + P.trash), ld);
 
   // per-lane cell sums: cells 0..31 and 32..63 (two arrays, so that each is
   // split into scalar registers)
@@ -1007,14 +955,13 @@ __global__ __launch_bounds__(kThreads) void line_wgrad(LineParams P, const T* __
   for (int n0 = n_begin; n0 < n_end; n0 += P.G) {
     const int ng = min(P.G, n_end - n0);
     const Frame f = frame_of(pg, P);
-    const Stage st = make_stage(P, opaque(&pg->vw), opaque(&pg->ks), opaque(&pg->ms));
     __syncthreads();
-    stage_store<T, S>(P, st, tiles + kGuard + P.halo * S + P.halo, P.PS, 0, f.tr != 0, px);
-    stage_store<T, S>(P, st, gtiles + 6, P.GPS, 0, f.tr != 0, pd);
+    stage_store<T, S>(lx, tr, px);
+    stage_store<T, S>(ld, tr, pd);
     __syncthreads();
     if (n0 + P.G < n_end) {
-      stage_load(P, st, xc + (size_t)(n0 + P.G) * img, min(P.G, n_end - n0 - P.G), px);
-      stage_load(P, st, dc + (size_t)(n0 + P.G) * img, min(P.G, n_end - n0 - P.G), pd);
+      stage_load(P, xc + (size_t)(n0 + P.G) * img, min(P.G, n_end - n0 - P.G), goff, px);
+      stage_load(P, dc + (size_t)(n0 + P.G) * img, min(P.G, n_end - n0 - P.G), goff, pd);
     }
     if (f.s == 0)
       wgrad_group<S, kRv, 0, KB>(P, f, task_map(P, f, lane), wave, tiles, gtiles, ng, pg, acc0, acc1);
