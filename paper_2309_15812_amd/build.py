@@ -42,7 +42,7 @@ def sources() -> list[str]:
 # such blocks would store a value before it arrives.  Their translation units
 # are therefore compiled with resource remarks and rejected if any kernel in
 # them uses scratch memory.
-CHECKED = "o1d_line_"
+CHECKED = ("o1d_line_", "o1d_strip_")
 REMARK = "-Rpass-analysis=kernel-resource-usage"
 
 

@@ -11,6 +11,7 @@
 #include "o1d_launch.h"
 #include "o1d_plan.h"
 #include "o1d_line.h"
+#include "o1d_strip.h"
 
 namespace {
 
@@ -96,7 +97,12 @@ o1d_status_t gather_entry(const char* fn, const void* in, const void* w, const f
   if (overlaps(in, bytes, out, bytes)) return fail(O1D_ERR_INVALID, "%s: output overlaps input", fn);
   (void)hipGetLastError();
   hipStream_t s = static_cast<hipStream_t>(stream);
-  const o1d::line::LinePlan lp = line_plan(N, C, H, W, K, sign, 0, vec_aligned(in, dt) && vec_aligned(out, dt));
+  const bool va = vec_aligned(in, dt) && vec_aligned(out, dt);
+  if (line_allowed()) {
+    const o1d::strip::Plan sp = o1d::strip::plan_strip(N, C, H, W, K, sign, va);
+    if (sp.ok) return hip_status(fn, o1d::launch_gather_strip((o1d::Dtype)dt, sp, in, w, theta, out, s));
+  }
+  const o1d::line::LinePlan lp = line_plan(N, C, H, W, K, sign, 0, va);
   if (lp.ok) return hip_status(fn, o1d::launch_gather_line((o1d::Dtype)dt, lp, in, w, theta, out, s));
   return hip_status(fn, o1d::launch_gather((o1d::Dtype)dt, in, w, theta, out, N, C, H, W, K, sign, s));
 }

@@ -12,6 +12,7 @@
 
 #include "o1d_launch.h"
 #include "o1d_plan.h"
+#include "o1d_strip.h"
 
 namespace o1d {
 namespace line {
@@ -172,17 +173,15 @@ inline LinePlan plan_line(int N, int C, int H, int W, int K, int sign, int kind,
   p.aux = kProgFloats + G * p.PS;
   p.red = p.aux + G * (kind == 0 ? p.OPS : p.GPS);
   p.trash = p.red + (kind == 1 ? kWaves * 64 : 0);
-  // images per workgroup: about three resident workgroups per CU over 256 CUs
+  // Images per workgroup for about three resident workgroups per CU (at
+  // most three by VGPRs, fewer when LDS runs out), fitted like the strip
+  // kernels' grids.  The choice depends on the sizes only, so the
+  // weight-gradient workspace size is a function of (N, C, H, W, K).
   const size_t lds = lds_for(G);
-  int per_cu = (int)(kMaxLdsBytes / lds);
+  int per_cu = strip::lds_resident(lds);
   if (per_cu > 3) per_cu = 3;
   if (per_cu < 1) per_cu = 1;
-  const long long planes = (long long)N * C;
-  int npw = (int)((planes + 256LL * per_cu - 1) / (256LL * per_cu));
-  if (const char* e = getenv("O1D_TUNE_NPW")) npw = atoi(e);
-  if (npw < 1) npw = 1;
-  npw = cdiv(npw, G) * G;
-  if (npw > cdiv(N, G) * G) npw = cdiv(N, G) * G;
+  const int npw = strip::fit_npw(N, C, G, 256LL * per_cu);
   p.npw = npw;
   pl.S = S;
   pl.KB = K <= 32 ? 32 : 64;

@@ -1,0 +1,202 @@
+// Host-side plan of the strip kernels: the forward pass and the input
+// gradient of the oriented 1D depthwise convolution for K <= 63 and planes
+// whose haloed tile fits in LDS.  The plan depends only on (N, C, H, W, K):
+// angles stay on the device and every workgroup derives its channel's line
+// itself, so the plan covers both staging frames (the plane and its
+// transpose) and both strip shapes (vertical and diagonal).
+#pragma once
+
+#include <stddef.h>
+#include <stdlib.h>
+
+#include "o1d_launch.h"
+#include "o1d_plan.h"
+
+namespace o1d {
+namespace strip {
+
+constexpr int kWaves = 2;
+constexpr int kThreads = 64 * kWaves;
+constexpr int kMaxTaps = 63;  // wave 0 builds the program with one tap per lane
+// Strip shapes: a lane computes NC adjacent strips of R outputs.  Vertical
+// strips step u = (1, 0) in the staging frame, diagonal ones u = (1, +-1).
+// The lanes of a half-wave read 32 distinct LDS banks: vertical strips sit
+// on consecutive columns; diagonal blocks (4 columns apart) are laid out as
+// 8 blocks x 4 bands per half-wave, the bands being 7 S (odd) rows apart.
+constexpr int kRv = 28, kNv = 1;
+constexpr int kRd = 7, kNd = 4;
+constexpr int kGuard = 16;       // floats before and after every tile slot
+constexpr int kProgWords = 208;  // the per-channel program in LDS
+constexpr int kMaxSlots = 8;     // staging slots (4 elements each) per lane and group
+constexpr size_t kLdsBudget = 64 * 1024;
+
+// Odd tile row strides compiled into the kernels: for an odd stride the
+// transposed staging accesses of a half-wave hit 32 distinct banks.
+#define O1D_STRIP_STRIDES(X) X(47) X(63) X(77) X(87) X(103) X(119) X(143)
+constexpr int kStrides[] = {47, 63, 77, 87, 103, 119, 143};
+
+__host__ __device__ inline int cdiv(int a, int b) { return (a + b - 1) / b; }
+
+// Workgroups of `lds_bytes` dynamic LDS that stay resident on one CU: LDS is
+// granted in 1 KB steps and a little of the 160 KB is not available, so five
+// workgroups of 32 KB do not fit (measured: four are resident).
+inline int lds_resident(size_t lds_bytes) {
+  const size_t granted = (lds_bytes + 1023) / 1024 * 1024;
+  return granted ? (int)((kMaxLdsBytes - 512) / granted) : 1;
+}
+
+// Images per workgroup (a multiple of G) for `slots` resident workgroups:
+// the grid of C * ceil(N / npw) workgroups runs in ceil(grid / slots)
+// rounds, each costing npw planes plus about 1.5 planes of workgroup set-up
+// (program, zeroed tile, the first group's exposed load); npw minimises
+// that, the most planes per workgroup among equals.
+inline int fit_npw(int N, int C, int G, long long slots) {
+  if (slots < 1) slots = 1;
+  double best = -1.0;
+  int npw = cdiv(N, G) * G;
+  for (int n = G; n <= cdiv(N, G) * G; n += G) {
+    const long long grid = (long long)C * cdiv(N, n);
+    const double span = (double)((grid + slots - 1) / slots) * (n + 1.5);
+    if (best < 0 || span <= best) {
+      best = span;
+      npw = n;
+    }
+  }
+  if (const char* e = getenv("O1D_TUNE_NPW"))
+    if (atoi(e) > 0) npw = cdiv(atoi(e), G) * G;
+  return npw;
+}
+
+// Task grid of one staging frame (Hs rows x Ws columns) for the strip shape
+// of step s: nb bands of R rows; strip columns j in [jlo, jlo + nj) (a
+// diagonal strip's R outputs cover columns j .. j + s (R - 1), so strips
+// start up to R - 1 columns outside the plane); ncg groups of NC adjacent
+// strips per band.  A task = one group of one band of one plane.
+// Lanes per plane (ppt): vertical tasks one per lane, band after band;
+// diagonal tasks in half-wave blocks of 8 column groups x 4 bands.
+struct Shape {
+  int R, NC, nb, nj, jlo, ncg, ppt;
+  int bq, bb;  // diagonal: half-wave blocks along the column groups and along the bands
+};
+
+__host__ __device__ inline Shape shape_of(int Hs, int Ws, int s) {
+  Shape t;
+  t.R = s ? kRd : kRv;
+  t.NC = s ? kNd : kNv;
+  t.nb = cdiv(Hs, t.R);
+  t.nj = Ws + (s ? t.R - 1 : 0);
+  t.jlo = s > 0 ? -(t.R - 1) : 0;
+  t.ncg = cdiv(t.nj, t.NC);
+  t.bq = cdiv(t.ncg, 8);
+  t.bb = cdiv(t.nb, 4);
+  t.ppt = s ? 32 * t.bq * t.bb : t.nb * t.ncg;
+  return t;
+}
+
+struct Params {
+  int N, C, H, W, K, sign;
+  int G;      // planes staged at once (one task per lane for all of them)
+  int npw;    // images per workgroup
+  int halo;   // zero rows above and below the plane in the tile
+  int mc;     // zero columns left and right of the plane in the tile
+  int TR;     // tile rows
+  int PS;     // floats per tile slot, guards included
+  int ks, ms; // staging grid per plane: steps of 8 kWaves rows, segments of 32 columns
+  int nq;     // staging slots per group = G ks ms
+  int trash;  // float offset of the trash area (writes of slots outside the plane)
+};
+
+struct Plan {
+  Params p{};
+  int S = 0;
+  int KB = 0;  // cell bound compiled into the walk: 32 or 64
+  int blocks_n = 0;
+  size_t lds_bytes = 0;
+  bool ok = false;
+};
+
+// vec_ok: tensors aligned for 4-element vector accesses.
+inline Plan plan_strip(int N, int C, int H, int W, int K, int sign, bool vec_ok) {
+  Plan pl;
+  if (K < 1 || K > kMaxTaps || N < 1 || C < 1 || H < 1 || W < 1) return pl;
+  if (W % 4 != 0 || !vec_ok) return pl;
+  const int M = H > W ? H : W;
+  const int halo = (K / 2) < (M - 1) ? (K / 2) : (M - 1);
+  const int mc = halo > kRd - 1 + kNd - 1 + 2 ? halo : kRd - 1 + kNd - 1 + 2;
+  int cover = 0, ppt = 0;
+  for (int f = 0; f < 2; ++f)
+    for (int s = 0; s < 2; ++s) {
+      const Shape t = shape_of(f ? W : H, f ? H : W, s);
+      if (t.nb * t.R > cover) cover = t.nb * t.R;
+      if (t.ppt > ppt) ppt = t.ppt;
+    }
+  int S = 0;
+  for (int s : kStrides)
+    if (s >= M + 2 * mc) {
+      S = s;
+      break;
+    }
+  if (S == 0) return pl;
+  Params& p = pl.p;
+  p.N = N; p.C = C; p.H = H; p.W = W; p.K = K; p.sign = sign;
+  p.halo = halo;
+  p.mc = mc;
+  p.TR = cover + 2 * halo;
+  p.PS = p.TR * S + 2 * kGuard;
+  p.ks = cdiv(H, 8 * kWaves);
+  p.ms = cdiv(W, 32);
+  const int per_plane_slots = p.ks * p.ms;
+  const int max_slots = kMaxSlots;
+  // planes per group: every task of the group on its own lane
+  int G = kThreads / ppt;
+  if (G < 1) return pl;
+  if (G > N) G = N;
+  if (G * per_plane_slots > max_slots) G = max_slots / per_plane_slots;
+  if (G < 1) return pl;
+  const int trash = 64 + 3 * S + 4;  // a word per lane plus the reach of a transposed vector write
+  auto lds_for = [&](int g) { return ((size_t)kProgWords + (size_t)g * p.PS + (size_t)trash) * 4; };
+  while (G > 1 && lds_for(G) > kLdsBudget) --G;
+  if (lds_for(G) > kMaxLdsBytes) return pl;
+  // buffer resources cover a group in bytes (float32 at most), below 2^31
+  const long long HW = (long long)H * W;
+  if ((long long)(G + 1) * C * HW * 4 >= (1ll << 31)) return pl;
+  p.G = G;
+  p.nq = G * per_plane_slots;
+  p.trash = kProgWords + G * p.PS;
+  // images per workgroup: a default from the LDS rule; the launcher refits
+  // it to the kernel's residency
+  const size_t lds = lds_for(G);
+  int per_cu = lds_resident(lds);
+  if (per_cu > 6) per_cu = 6;
+  const int npw = fit_npw(N, C, G, 256LL * (per_cu < 1 ? 1 : per_cu));
+  p.npw = npw;
+  pl.S = S;
+  pl.KB = K <= 32 ? 32 : 64;
+  pl.blocks_n = cdiv(N, npw);
+  pl.lds_bytes = lds;
+  pl.ok = true;
+  return pl;
+}
+
+}  // namespace strip
+
+// One translation unit per storage type and cell bound; see o1d_strip_kernels.h.
+#define O1D_STRIP_DECL(NAME)                                                                                   \
+  hipError_t NAME(const strip::Plan& pl, const void* in, const void* w, const float* theta, void* out, \
+                  hipStream_t stream);
+O1D_STRIP_DECL(launch_gather_strip_f32_k32)
+O1D_STRIP_DECL(launch_gather_strip_f32_k64)
+O1D_STRIP_DECL(launch_gather_strip_bf16_k32)
+O1D_STRIP_DECL(launch_gather_strip_bf16_k64)
+#undef O1D_STRIP_DECL
+
+inline hipError_t launch_gather_strip(Dtype dt, const strip::Plan& pl, const void* in, const void* w,
+                                      const float* theta, void* out, hipStream_t stream) {
+  if (dt == Dtype::F32)
+    return pl.KB == 32 ? launch_gather_strip_f32_k32(pl, in, w, theta, out, stream)
+                       : launch_gather_strip_f32_k64(pl, in, w, theta, out, stream);
+  return pl.KB == 32 ? launch_gather_strip_bf16_k32(pl, in, w, theta, out, stream)
+                     : launch_gather_strip_bf16_k64(pl, in, w, theta, out, stream);
+}
+
+}  // namespace o1d

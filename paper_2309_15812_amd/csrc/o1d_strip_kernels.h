@@ -1,0 +1,586 @@
+// Device code of the strip kernels (included by the per-storage-type
+// translation units o1d_strip_gather_{f32,bf16}.hip).
+//
+// Strip kernels: forward pass and input gradient of the oriented 1D
+// depthwise convolution (Eq. 1: y[p,q] = sum_k w_k x[p + dh_k, q + dw_k],
+// offsets from Eq. 2) on gfx950.
+//
+// For one channel every output reads the same cells, the digital line of
+// Eq. (2) shifted to the output.  A workgroup stages planes of its channel
+// in LDS with a zero margin (the paper's one-read staging of the input in
+// on-chip memory), then every lane computes a block of outputs: NC adjacent
+// strips of R outputs each, the strips stepping u = (1, s), s in {-1, 0, 1},
+// in the staging frame.  Walking the line's cells in order, a cell that is
+// its predecessor moved by u (a continuing cell) needs the lane's previous
+// window moved by one row: R + 1 register rows rotate, and only the new
+// row (NC values) is read.  A cell that starts a run reloads all R rows.
+// Each cell then costs NC LDS reads and R * NC FMAs, and its bookkeeping is
+// a handful of instructions:
+//  * run base addresses: the LDS address of row i, column k of cell c is
+//    base_run + 4 ((c + i) st + k), st = the strip step in floats, so the
+//    offsets are immediates and only a run's first cell computes a base;
+//  * the next cell's new row is read before the cell's multiplies.
+// The issue rate of a SIMD (about one instruction per four cycles) bounds
+// these kernels, so the multiplies' share of the instruction stream is
+// what the design maximises.
+//
+// Geometry per channel, built once per workgroup by wave 0 (one tap per
+// lane): the staging frame (the plane, or its transpose when the line spans
+// more columns than rows, so that the line advances by at least one row per
+// cell), the cells (duplicate taps merged with their weights added, taps
+// that never land in the plane dropped), the strip step s (the most frequent
+// row-advancing step between cells), per cell its run offset and weight,
+// and the run starts.
+//
+// Outputs leave through LDS: after the walk the lanes write their blocks
+// into the tile (frame orientation, zero outside the plane so that the
+// margins stay zero), and the staging lane layout stores them as coalesced
+// rows of the plane.
+#pragma once
+
+#include <hip/hip_runtime.h>
+#include <stdint.h>
+
+#include <atomic>
+#include <utility>
+
+#include "o1d_device.h"
+#include "o1d_launch.h"
+#include "o1d_strip.h"
+#include "o1d_strip_asm.h"
+
+namespace o1d {
+namespace strip {
+namespace {
+
+template <class F, int... I>
+__device__ __forceinline__ void static_for_impl(F&& f, std::integer_sequence<int, I...>) {
+  (f(std::integral_constant<int, I>{}), ...);
+}
+template <int N, class F>
+__device__ __forceinline__ void static_for(F&& f) {
+  static_for_impl(f, std::make_integer_sequence<int, N>{});
+}
+
+// ---------------------------------------------------------------- program
+
+struct Prog {
+  int tr;      // staging frame = transposed plane
+  int s;       // strip step u = (1, s) in the staging frame
+  int ncells;
+  int finite;  // the channel's angle is finite
+  int pad0_[4];
+  uint32_t brk[2];  // bit c: cell c starts a run
+  int pad1_[6];
+  int rbase[64];     // run offset of cell c in bytes: 4 (off_c - c st), off_c = a S + b in the frame
+  float w[64];       // weight of cell c (duplicate taps summed)
+  int tap_cell[64];  // walk cell of every tap, -1 if the tap never lands in the plane
+};
+static_assert(sizeof(Prog) == kProgWords * 4, "kProgWords must match the program layout");
+
+__device__ __forceinline__ int wave_min_i(int v) {
+#pragma unroll
+  for (int m = 32; m >= 1; m >>= 1) v = min(v, __shfl_xor(v, m, 64));
+  return v;
+}
+__device__ __forceinline__ int wave_max_i(int v) {
+#pragma unroll
+  for (int m = 32; m >= 1; m >>= 1) v = max(v, __shfl_xor(v, m, 64));
+  return v;
+}
+__device__ __forceinline__ uint64_t wave_or(uint64_t m) {
+#pragma unroll
+  for (int i = 32; i >= 1; i >>= 1) {
+    const uint32_t lo = __shfl_xor((uint32_t)m, i, 64), hi = __shfl_xor((uint32_t)(m >> 32), i, 64);
+    m |= ((uint64_t)hi << 32) | lo;
+  }
+  return m;
+}
+__device__ __forceinline__ uint64_t below_mask(int n) { return n <= 0 ? 0ull : (n >= 64 ? ~0ull : (~0ull >> (64 - n))); }
+__device__ __forceinline__ uint64_t above_mask(int n) { return n >= 63 ? 0ull : (~0ull << (n + 1)); }
+__device__ __forceinline__ int popc(uint64_t m) { return __popcll(m); }
+__device__ __forceinline__ int hibit(uint64_t m) { return m ? 63 - __clzll(m) : -1; }
+__device__ __forceinline__ int lobit(uint64_t m) { return m ? __ffsll((long long)m) - 1 : 64; }
+
+// Builds the channel's program.  Called by the 64 lanes of wave 0, lane k =
+// tap k (K <= 63).  sign = -1 negates the offsets (input gradient: the
+// adjoint of Eq. 1 in x is the same gather with mirrored taps).  Taps move
+// monotonically along the line, so taps on one pixel are consecutive (and
+// at most two, max(|sin|, |cos|) >= 1/sqrt(2)) and the taps that can land
+// in the plane form one contiguous range.
+template <typename T>
+__device__ void build_prog(Prog* pg, const T* __restrict__ wgt, float theta, int c, int K, int sign, int H, int W,
+                           int S) {
+  const int k = threadIdx.x;
+  const bool act = k < K;
+  int dh = 0, dw = 0;
+  bool fin = true;
+  float wk = 0.f;
+  if (act) {
+    fin = tap_offset(theta, K, k, &dh, &dw);
+    dh *= sign;
+    dw *= sign;
+    if (wgt) wk = to_f32(wgt[(size_t)c * K + k]);
+  }
+  const int hmin = wave_min_i(act ? dh : 1 << 20), hmax = wave_max_i(act ? dh : -(1 << 20));
+  const int wmin = wave_min_i(act ? dw : 1 << 20), wmax = wave_max_i(act ? dw : -(1 << 20));
+  const bool tr = (wmax - wmin) > (hmax - hmin);
+  const int a = tr ? dw : dh;  // row offset in the staging frame
+  const int b = tr ? dh : dw;  // column offset in the staging frame
+  const int Hs = tr ? W : H, Ws = tr ? H : W;
+  const bool keep = act && a > -Hs && a < Hs && b > -Ws && b < Ws;
+  const uint64_t keptm = __ballot(keep);
+
+  // duplicates: the previous kept tap on the same pixel; the first tap of a
+  // pair carries the summed weight
+  const int pk = hibit(keptm & below_mask(k));
+  const int pa = __shfl(a, pk < 0 ? 0 : pk, 64), pb = __shfl(b, pk < 0 ? 0 : pk, 64);
+  const bool dup = keep && pk >= 0 && pa == a && pb == b;
+  const uint64_t dupm = __ballot(dup);
+  const int nk = lobit(keptm & above_mask(k));
+  const float nw = __shfl(wk, nk > 63 ? 63 : nk, 64);
+  const bool next_dup = nk < 64 && ((dupm >> nk) & 1ull);
+  const float cw = wk + (next_dup ? nw : 0.f);
+  const bool cell = keep && !dup;
+  const uint64_t cellm = __ballot(cell);
+  const int ncells = popc(cellm);
+  const int ci = popc(cellm & below_mask(k));
+
+  // cell order: frame rows increasing
+  const int lfirst = lobit(cellm), llast = hibit(cellm);
+  const int a_first = __shfl(a, lfirst > 63 ? 0 : lfirst, 64), a_last = __shfl(a, llast < 0 ? 0 : llast, 64);
+  const bool rev = a_last < a_first;
+  const int co = rev ? ncells - 1 - ci : ci;
+  const int pc = rev ? lobit(cellm & above_mask(k)) : hibit(cellm & below_mask(k));  // predecessor cell lane
+  const bool hp = cell && pc >= 0 && pc < 64;
+  const int qa = __shfl(a, hp ? pc : 0, 64), qb = __shfl(b, hp ? pc : 0, 64);
+  const int da = a - qa, db = b - qb;
+  const int n0 = popc(__ballot(hp && da == 1 && db == 0));
+  const int np = popc(__ballot(hp && da == 1 && db == 1));
+  const int nm = popc(__ballot(hp && da == 1 && db == -1));
+  int s = 0;
+  if (np > n0 && np >= nm)
+    s = 1;
+  else if (nm > n0 && nm > np)
+    s = -1;
+  const bool cont = hp && da == 1 && db == s;
+  const bool allfin = __ballot(act && !fin) == 0ull;
+
+  // walk cell of this lane's cell
+  const int cw_idx = co;
+  const int st = S + s;
+  pg->rbase[k] = 0;
+  pg->w[k] = 0.f;
+  if (cell && cw_idx >= 0 && cw_idx < 64) {
+    pg->rbase[cw_idx] = 4 * ((a * S + b) - cw_idx * st);
+    pg->w[cw_idx] = allfin ? cw : __builtin_nanf("");  // a non-finite angle poisons the channel
+  }
+  const uint64_t brk = wave_or((cell && !cont && cw_idx >= 0 && cw_idx < 64) ? (1ull << cw_idx) : 0ull);
+  const int own = dup ? pk : k;  // the lane of the cell that owns this tap
+  const int ocw = __shfl(cw_idx, own < 0 ? 0 : own, 64);
+  if (act) pg->tap_cell[k] = keep ? ocw : -1;
+  if (k == 0) {
+    pg->brk[0] = (uint32_t)brk;
+    pg->brk[1] = (uint32_t)(brk >> 32);
+    pg->ncells = ncells;
+    pg->tr = tr ? 1 : 0;
+    pg->s = s;
+    pg->finite = allfin ? 1 : 0;
+  }
+}
+
+// ---------------------------------------------------------------- walk
+
+__device__ __forceinline__ uint32_t lds_addr(const float* p) {
+  return (uint32_t)(uintptr_t)(const __attribute__((address_space(3))) float*)p;
+}
+__device__ __forceinline__ float lds_load(uint32_t a) {
+  return *(const __attribute__((address_space(3))) float*)(uintptr_t)a;
+}
+__device__ __forceinline__ void lds_store(uint32_t a, float v) {
+  *(__attribute__((address_space(3))) float*)(uintptr_t)a = v;
+}
+
+// One cell of the gather walk: the window step (generated inline assembly)
+// and the cell's R * NC multiplies.
+template <int R, int NC, int ST, int C, int KB>
+__device__ __forceinline__ void gather_cell(float (&sl)[R + 1][NC], uint32_t& base, uint32_t lb, uint32_t vrb,
+                                            uint32_t bits, uint32_t vw, float (&acc)[R][NC]) {
+  constexpr bool kLast = C + 1 == KB;
+  if constexpr (R == kRv && NC == kNv) {
+    if constexpr (kLast)
+      cell_asm_28x1_last<ST, C>(sl, base, lb, vrb, bits);
+    else
+      cell_asm_28x1<ST, C>(sl, base, lb, vrb, bits);
+  } else {
+    static_assert(R == kRd && NC == kNd, "strip shape without a generated window step");
+    if constexpr (kLast)
+      cell_asm_7x4_last<ST, C>(sl, base, lb, vrb, bits);
+    else
+      cell_asm_7x4<ST, C>(sl, base, lb, vrb, bits);
+  }
+  const float wc = __int_as_float(__builtin_amdgcn_readlane((int)vw, C));
+#pragma unroll
+  for (int i = 0; i < R; ++i)
+#pragma unroll
+    for (int k = 0; k < NC; ++k) acc[i][k] = fmaf(wc, sl[(C + i) % (R + 1)][k], acc[i][k]);
+}
+
+// acc[i][k] += sum over the cells c of w_c * x[cell c + i u + (0, k)]: the
+// walk of one block over cells C .. ncells - 1.
+template <int R, int NC, int ST, int C, int KB>
+struct GatherWalk {
+  static __device__ __forceinline__ void run(int n, uint32_t& base, uint32_t lb, uint32_t vrb, uint32_t bits_lo,
+                                             uint32_t bits_hi, uint32_t vw, float (&sl)[R + 1][NC],
+                                             float (&acc)[R][NC]) {
+    // the cell count passes through an empty asm statement, so that the
+    // test stays one scalar compare here (instead of a precomputed mask per
+    // cell, which costs scalar registers and reads)
+    int nn = n;
+    asm volatile("" : "+s"(nn));
+    if (C >= nn) return;
+    gather_cell<R, NC, ST, C, KB>(sl, base, lb, vrb, C < 32 ? bits_lo : bits_hi, vw, acc);
+    GatherWalk<R, NC, ST, C + 1, KB>::run(n, base, lb, vrb, bits_lo, bits_hi, vw, sl, acc);
+  }
+};
+template <int R, int NC, int ST, int KB>
+struct GatherWalk<R, NC, ST, KB, KB> {
+  static __device__ __forceinline__ void run(int, uint32_t&, uint32_t, uint32_t, uint32_t, uint32_t, uint32_t,
+                                             float (&)[R + 1][NC], float (&)[R][NC]) {}
+};
+
+// ---------------------------------------------------------------- staging
+
+// Staging of a plane group through registers.  Every lane moves 4
+// consecutive elements of a plane row per slot with one 16-byte (bfloat16:
+// 8-byte) buffer access.  A half-wave covers 4 rows x 8 quads: lane -> row
+// (lane >> 3) & 3 (+4 in the second half-wave, +8 per wave), quad lane & 7.
+// For an odd tile row stride the 32 component writes of a half-wave then hit
+// 32 distinct banks in either frame.  Slot q = (g, k, m): plane g of the
+// group, row step k (8 kWaves rows), column segment m (32 columns).
+//
+// Every lane runs all kMaxSlots slots (slots past the group read zeros,
+// store nothing and write the trash area), so that no register is written
+// conditionally.  A lane's slot addresses are computed once per workgroup:
+//  * goff[q]: byte offset of its 4 elements from the group's first element,
+//    or kOob for a slot outside the plane; buffer accesses beyond the
+//    resource's size read zeros and drop stores;
+//  * lt[q]: LDS address of the first element in the tile (frame orientation),
+//    or of the lane's word in the trash area for a slot outside the plane.
+constexpr uint32_t kOob = 0x80000000u;
+
+template <int NQ, class F>
+__device__ __forceinline__ void for_each_slot(const Params& P, F&& f) {
+  const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6;
+  const int hr = wave * 8 + (lane >> 5) * 4 + ((lane >> 3) & 3);
+  const int w0 = 4 * (lane & 7);
+  const int per = P.ks * P.ms;
+  static_for<NQ>([&](auto qc) __attribute__((always_inline)) {
+    constexpr int q = decltype(qc)::value;
+    const int g = q / per, r = q - g * per, kk = r / P.ms, m = r - kk * P.ms;
+    const int h = hr + 8 * kWaves * kk, w = w0 + 32 * m;
+    f(q, q < P.nq && g < P.G && h < P.H && w < P.W, g, h, w);
+  });
+}
+
+template <typename T>
+struct Raw;
+template <>
+struct Raw<float> {
+  static constexpr int kWords = 4;
+  static __device__ __forceinline__ void load(__amdgpu_buffer_rsrc_t rs, uint32_t off, uint32_t* r) {
+    const auto v = __builtin_amdgcn_raw_buffer_load_b128(rs, off, 0, 0);
+    r[0] = v[0]; r[1] = v[1]; r[2] = v[2]; r[3] = v[3];
+  }
+  static __device__ __forceinline__ float elem(const uint32_t* r, int j) { return __uint_as_float(r[j]); }
+  static __device__ __forceinline__ void store(__amdgpu_buffer_rsrc_t rs, uint32_t off, const float* e) {
+    typedef unsigned int u4 __attribute__((ext_vector_type(4)));
+    u4 v;
+    v[0] = __float_as_uint(e[0]); v[1] = __float_as_uint(e[1]); v[2] = __float_as_uint(e[2]); v[3] = __float_as_uint(e[3]);
+    __builtin_amdgcn_raw_buffer_store_b128(v, rs, off, 0, 0);
+  }
+};
+template <>
+struct Raw<uint16_t> {
+  static constexpr int kWords = 2;
+  static __device__ __forceinline__ void load(__amdgpu_buffer_rsrc_t rs, uint32_t off, uint32_t* r) {
+    const auto v = __builtin_amdgcn_raw_buffer_load_b64(rs, off, 0, 0);
+    r[0] = v[0]; r[1] = v[1];
+  }
+  static __device__ __forceinline__ float elem(const uint32_t* r, int j) {
+    const uint32_t w = r[j >> 1];
+    return __uint_as_float((j & 1) ? (w & 0xffff0000u) : (w << 16));
+  }
+  static __device__ __forceinline__ void store(__amdgpu_buffer_rsrc_t rs, uint32_t off, const float* e) {
+    typedef unsigned int u2 __attribute__((ext_vector_type(2)));
+    u2 v;
+    v[0] = (uint32_t)from_f32<uint16_t>(e[0]) | ((uint32_t)from_f32<uint16_t>(e[1]) << 16);
+    v[1] = (uint32_t)from_f32<uint16_t>(e[2]) | ((uint32_t)from_f32<uint16_t>(e[3]) << 16);
+    __builtin_amdgcn_raw_buffer_store_b64(v, rs, off, 0, 0);
+  }
+};
+
+// A buffer resource over `bytes` bytes from p (raw, no swizzle).
+__device__ __forceinline__ __amdgpu_buffer_rsrc_t buffer_of(const void* p, int bytes) {
+  return __builtin_amdgcn_make_buffer_rsrc(const_cast<void*>(p), (short)0, bytes, 0x00020000);
+}
+
+template <typename T>
+struct Stage {
+  static constexpr int kQ = kMaxSlots;
+  static constexpr int kWords = kMaxSlots * Raw<T>::kWords;  // staging registers per group
+  uint32_t goff[kQ];
+  uint32_t lt[kQ];
+
+  __device__ __forceinline__ void init_global(const Params& P) {
+    const int img = P.C * P.H * P.W;
+    for_each_slot<kQ>(P, [&](int q, bool ok, int g, int h, int w) __attribute__((always_inline)) {
+      goff[q] = ok ? (uint32_t)((g * img + h * P.W + w) * (int)sizeof(T)) : kOob;
+    });
+  }
+  __device__ __forceinline__ void init_lds(const Params& P, int S, bool tr, uint32_t tiles, uint32_t trash) {
+    const uint32_t tl = trash + 4 * (threadIdx.x & 63);
+    for_each_slot<kQ>(P, [&](int q, bool ok, int g, int h, int w) __attribute__((always_inline)) {
+      const int r = tr ? w : h, c = tr ? h : w;
+      lt[q] = ok ? tiles + 4 * (uint32_t)(g * P.PS + kGuard + (P.halo + r) * S + P.mc + c) : tl;
+    });
+  }
+  // Loads the group's slots (ng >= 1 planes from src) into raw registers.
+  // ng = 0 reads zeros without touching memory (an empty buffer range).
+  __device__ __forceinline__ void load(const Params& P, const T* src, int ng, uint32_t (&v)[kWords]) const {
+    const __amdgpu_buffer_rsrc_t rs = buffer_of(src, ng * P.C * P.H * P.W * (int)sizeof(T));
+    // every slot, so that each register is written unconditionally (slots
+    // past the group read zeros at offset kOob)
+#pragma unroll
+    for (int q = 0; q < kQ; ++q) Raw<T>::load(rs, goff[q], &v[Raw<T>::kWords * q]);
+  }
+  // Writes the slots into the tile: the 4 elements of a slot are consecutive
+  // along the frame's rows, or along its columns (stride S) when transposed.
+  __device__ __forceinline__ void store_lds(const Params& P, int S, bool tr, const uint32_t (&v)[kWords]) const {
+    const uint32_t step = tr ? 4u * S : 4u;
+#pragma unroll
+    for (int q = 0; q < kQ; ++q)
+#pragma unroll
+      for (int j = 0; j < 4; ++j) lds_store(lt[q] + j * step, Raw<T>::elem(&v[Raw<T>::kWords * q], j));
+  }
+  // Reads the tile's outputs (frame orientation) in the slot layout.
+  __device__ __forceinline__ void read_lds(const Params& P, int S, bool tr, float (&e)[kQ][4]) const {
+    const uint32_t step = tr ? 4u * S : 4u;
+#pragma unroll
+    for (int q = 0; q < kQ; ++q)
+#pragma unroll
+      for (int j = 0; j < 4; ++j) e[q][j] = lds_load(lt[q] + j * step);
+  }
+  __device__ __forceinline__ void store(const Params& P, T* dst, int ng, const float (&e)[kQ][4]) const {
+    const __amdgpu_buffer_rsrc_t rs = buffer_of(dst, ng * P.C * P.H * P.W * (int)sizeof(T));
+#pragma unroll
+    for (int q = 0; q < kQ; ++q) Raw<T>::store(rs, goff[q], e[q]);
+  }
+};
+
+// ---------------------------------------------------------------- forward / input gradient
+
+struct Chan {
+  int tr, s, ncells, Hs, Ws;
+  uint32_t bits_lo, bits_hi, vrb, vw;
+};
+
+// The group loop of one workgroup for the channel's strip shape (R, NC, SD).
+template <typename T, int S, int KB, int R, int NC, int SD>
+__device__ __forceinline__ void gather_groups(const Params& P, const Chan& ch, float* smem, const T* inc, T* outc,
+                                              int n_begin, int n_end, Stage<T>& stg, uint32_t (&pre)[Stage<T>::kWords]) {
+  constexpr int ST = S + SD;
+  const Shape sh = shape_of(ch.Hs, ch.Ws, SD);
+  const size_t img = (size_t)P.C * P.H * P.W;
+  float* tiles = smem + kProgWords;
+  // this lane's block: plane g of the group, rows b0 .. b0 + R - 1, strip columns j0 .. j0 + NC - 1
+  const int t = threadIdx.x;
+  int g = t / sh.ppt;
+  const int r = t - g * sh.ppt;
+  int band, cg;
+  if (SD == 0) {
+    band = r / sh.ncg;
+    cg = r - band * sh.ncg;
+  } else {
+    const int blk = r >> 5, bqi = blk % sh.bq, bbi = blk / sh.bq;
+    cg = 8 * bqi + (r & 7);
+    band = 4 * bbi + ((r >> 3) & 3);
+  }
+  const bool task = g < P.G && band < sh.nb && cg < sh.ncg;
+  if (!task) g = 0;
+  const int b0 = task ? band * R : 0;
+  const int j0 = task ? sh.jlo + cg * NC : sh.jlo;
+  const uint32_t lb = lds_addr(tiles + g * P.PS + kGuard + (P.halo + b0) * S + P.mc + j0);
+  // outputs outside the plane are written as zeros (into the tile's margins)
+  bool full = b0 + R <= ch.Hs;
+  const int cmin = j0 + (SD < 0 ? -(R - 1) : 0), cmax = j0 + NC - 1 + (SD > 0 ? R - 1 : 0);
+  full = full && cmin >= 0 && cmax < ch.Ws;
+
+  for (int n0 = n_begin; n0 < n_end; n0 += P.G) {
+    const int ng = min(P.G, n_end - n0);
+    // the next group's loads (none past the end: an empty range, so that the
+    // prefetch registers are written unconditionally and never copied)
+    const int nn = max(0, min(P.G, n_end - n0 - P.G));
+    stg.load(P, inc + (size_t)(nn > 0 ? n0 + P.G : n_begin) * img, nn, pre);
+    float acc[R][NC];
+#pragma unroll
+    for (int i = 0; i < R; ++i)
+#pragma unroll
+      for (int k = 0; k < NC; ++k) acc[i][k] = 0.f;
+    // the window's register rows: the walk's first cell loads all of them
+    float sl[R + 1][NC];
+    uint32_t base = lb;
+    GatherWalk<R, NC, ST, 0, KB>::run(ch.ncells, base, lb, ch.vrb, ch.bits_lo, ch.bits_hi, ch.vw, sl, acc);
+    // the last cell's read-ahead (of a cell that does not exist) may still be in flight
+    asm volatile("s_waitcnt lgkmcnt(0)" ::: "memory");
+    __syncthreads();  // every lane has finished reading the tile
+    if (task && g < ng) {
+      if (full) {
+#pragma unroll
+        for (int i = 0; i < R; ++i)
+#pragma unroll
+          for (int k = 0; k < NC; ++k) lds_store(lb + 4 * (i * ST + k), acc[i][k]);
+      } else {
+#pragma unroll
+        for (int i = 0; i < R; ++i)
+#pragma unroll
+          for (int k = 0; k < NC; ++k) {
+            const int col = j0 + SD * i + k;
+            const bool in = b0 + i < ch.Hs && col >= 0 && col < ch.Ws;
+            lds_store(lb + 4 * (i * ST + k), in ? acc[i][k] : 0.f);
+          }
+      }
+    }
+    __syncthreads();  // the group's outputs are in the tile
+    float e[Stage<T>::kQ][4];
+    stg.read_lds(P, S, ch.tr != 0, e);
+    __syncthreads();  // the tile is free
+    stg.store_lds(P, S, ch.tr != 0, pre);  // past the end: zeros into a tile nobody reads
+    stg.store(P, outc + (size_t)n0 * img, ng, e);
+    __syncthreads();  // the next group is staged
+  }
+}
+
+template <typename T, int S, int KB>
+__global__ __launch_bounds__(kThreads) void strip_gather(Params P, const T* __restrict__ in, const T* __restrict__ wgt,
+                                                         const float* __restrict__ theta, T* __restrict__ out) {
+  extern __shared__ float smem[];
+  Prog* pg = reinterpret_cast<Prog*>(smem);
+  float* tiles = smem + kProgWords;
+  const int c = blockIdx.y;
+  const int tid = threadIdx.x;
+  const int wave = __builtin_amdgcn_readfirstlane(tid >> 6);
+  const size_t HW = (size_t)P.H * P.W;
+  const size_t img = (size_t)P.C * HW;
+  const int n_begin = blockIdx.x * P.npw;
+  const int n_end = min(P.N, n_begin + P.npw);
+  const T* inc = in + (size_t)c * HW;
+  T* outc = out + (size_t)c * HW;
+
+  // The first group's loads do not depend on the frame: issue them first.
+  Stage<T> stg;
+  stg.init_global(P);
+  uint32_t pre[Stage<T>::kWords];
+  stg.load(P, inc + (size_t)n_begin * img, min(P.G, n_end - n_begin), pre);
+  for (int i = tid; i < P.G * P.PS; i += kThreads) tiles[i] = 0.f;  // margins and guards stay zero
+  if (wave == 0) build_prog<T>(pg, wgt, theta[c], c, P.K, P.sign, P.H, P.W, S);
+  __syncthreads();
+  Chan ch;
+  ch.tr = __builtin_amdgcn_readfirstlane(pg->tr);
+  ch.s = __builtin_amdgcn_readfirstlane(pg->s);
+  ch.ncells = min(__builtin_amdgcn_readfirstlane(pg->ncells), KB);
+  ch.bits_lo = __builtin_amdgcn_readfirstlane(pg->brk[0]);
+  ch.bits_hi = __builtin_amdgcn_readfirstlane(pg->brk[1]);
+  ch.vrb = (uint32_t)pg->rbase[tid & 63];
+  ch.vw = __float_as_uint(pg->w[tid & 63]);
+  ch.Hs = ch.tr ? P.W : P.H;
+  ch.Ws = ch.tr ? P.H : P.W;
+  stg.init_lds(P, S, ch.tr != 0, lds_addr(tiles), lds_addr(smem + P.trash));
+  stg.store_lds(P, S, ch.tr != 0, pre);
+  __syncthreads();
+  if (ch.s == 0)
+    gather_groups<T, S, KB, kRv, kNv, 0>(P, ch, smem, inc, outc, n_begin, n_end, stg, pre);
+  else if (ch.s > 0)
+    gather_groups<T, S, KB, kRd, kNd, 1>(P, ch, smem, inc, outc, n_begin, n_end, stg, pre);
+  else
+    gather_groups<T, S, KB, kRd, kNd, -1>(P, ch, smem, inc, outc, n_begin, n_end, stg, pre);
+}
+
+// ---------------------------------------------------------------- launch
+
+// Fits the grid to `per_cu` resident workgroups on every CU of the device.
+inline void fit_grid(Plan& pl, int per_cu) {
+  static std::atomic<int> cu_count{0};
+  int cus = cu_count.load(std::memory_order_relaxed);
+  if (cus == 0) {
+    int dev = 0, n = 0;
+    if (hipGetDevice(&dev) == hipSuccess && hipDeviceGetAttribute(&n, hipDeviceAttributeMultiprocessorCount, dev) ==
+                                                 hipSuccess && n > 0)
+      cus = n;
+    else
+      cus = 256;
+    cu_count.store(cus, std::memory_order_relaxed);
+  }
+  pl.p.npw = fit_npw(pl.p.N, pl.p.C, pl.p.G, (long long)cus * (per_cu < 1 ? 1 : per_cu));
+  pl.blocks_n = cdiv(pl.p.N, pl.p.npw);
+}
+
+// Resident workgroups per CU of strip_gather<T, S, KB> for a dynamic LDS
+// size.  The answer is cached per instantiation (the queries cost more host
+// time than a launch), packed with its LDS size into one atomic word.
+template <typename T, int S, int KB>
+hipError_t resident_per_cu(size_t lds_bytes, int* per_cu) {
+  static std::atomic<unsigned long long> cache{0};
+  const unsigned long long c = cache.load(std::memory_order_relaxed);
+  if (c != 0 && (c >> 8) == lds_bytes) {
+    *per_cu = (int)(c & 0xff);
+    return hipSuccess;
+  }
+  const void* fn = reinterpret_cast<const void*>(strip_gather<T, S, KB>);
+  hipError_t e = hipFuncSetAttribute(fn, hipFuncAttributeMaxDynamicSharedMemorySize, (int)kMaxLdsBytes);
+  if (e != hipSuccess) return e;
+  hipFuncAttributes fa;
+  e = hipFuncGetAttributes(&fa, fn);
+  if (e != hipSuccess) return e;
+  // Residency from the kernel's resources: waves per SIMD from its VGPRs
+  // (512 per lane, granules of 8, at most 8 waves), and the LDS rule of
+  // lds_resident.
+  const int vg = ((fa.numRegs > 0 ? fa.numRegs : 1) + 7) / 8 * 8;
+  int waves = 512 / vg;
+  if (waves > 8) waves = 8;
+  int n = 4 * waves / kWaves;
+  const int by_lds = lds_resident(lds_bytes);
+  if (by_lds < n) n = by_lds;
+  n = n < 1 ? 1 : (n > 255 ? 255 : n);
+  cache.store(((unsigned long long)lds_bytes << 8) | (unsigned long long)n, std::memory_order_relaxed);
+  *per_cu = n;
+  return hipSuccess;
+}
+
+template <typename T, int S, int KB>
+hipError_t gather_launch(const Plan& plan, const void* in, const void* w, const float* theta, void* out,
+                         hipStream_t stream) {
+  int per_cu = 0;
+  hipError_t e = resident_per_cu<T, S, KB>(plan.lds_bytes, &per_cu);
+  if (e != hipSuccess) return e;
+  Plan pl = plan;
+  fit_grid(pl, per_cu);
+  hipLaunchKernelGGL((strip_gather<T, S, KB>), dim3((unsigned)pl.blocks_n, (unsigned)pl.p.C, 1), dim3(kThreads),
+                     pl.lds_bytes, stream, pl.p, static_cast<const T*>(in), static_cast<const T*>(w), theta,
+                     static_cast<T*>(out));
+  return hipGetLastError();
+}
+
+template <typename T, int KB>
+hipError_t gather_t(const Plan& pl, const void* in, const void* w, const float* theta, void* out,
+                    hipStream_t stream) {
+#define O1D_CASE(SV) \
+  if (pl.S == SV) return gather_launch<T, SV, KB>(pl, in, w, theta, out, stream);
+  O1D_STRIP_STRIDES(O1D_CASE)
+#undef O1D_CASE
+  return hipErrorInvalidValue;
+}
+
+}  // namespace
+}  // namespace strip
+}  // namespace o1d
