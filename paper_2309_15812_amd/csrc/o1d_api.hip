@@ -72,7 +72,20 @@ bool vec_aligned(const void* p, o1d_dtype_t dt) { return ((uintptr_t)p % (dt == 
 // The workspace size must not depend on pointer alignment: take the larger
 // partial count of the kernels that aligned and unaligned tensors select
 // (the line kernels need aligned tensors; otherwise the tiled kernels run).
+o1d::strip::Plan strip_wgrad_plan(int N, int C, int H, int W, int K, bool vec_ok) {
+  if (!line_allowed()) return o1d::strip::Plan();
+  return o1d::strip::plan_strip(N, C, H, W, K, 1, 1, vec_ok);
+}
+
 size_t wgrad_workspace(int N, int C, int H, int W, int K) {
+  const o1d::strip::Plan sa = strip_wgrad_plan(N, C, H, W, K, true);
+  if (sa.ok) {
+    // aligned tensors take the strip kernel, unaligned ones a line or tiled kernel
+    const o1d::line::LinePlan b = line_plan(N, C, H, W, K, 1, 1, false);
+    const size_t pb = b.ok ? (size_t)b.blocks_n : o1d::plan_wgrad(N, C, H, W, K).parts();
+    const size_t parts = (size_t)sa.blocks_n > pb ? (size_t)sa.blocks_n : pb;
+    return parts * (size_t)C * (size_t)K * sizeof(float);
+  }
   const o1d::line::LinePlan a = line_plan(N, C, H, W, K, 1, 1, true);
   const o1d::line::LinePlan b = line_plan(N, C, H, W, K, 1, 1, false);
   const size_t tiled = o1d::plan_wgrad(N, C, H, W, K).parts();
@@ -99,7 +112,7 @@ o1d_status_t gather_entry(const char* fn, const void* in, const void* w, const f
   hipStream_t s = static_cast<hipStream_t>(stream);
   const bool va = vec_aligned(in, dt) && vec_aligned(out, dt);
   if (line_allowed()) {
-    const o1d::strip::Plan sp = o1d::strip::plan_strip(N, C, H, W, K, sign, va);
+    const o1d::strip::Plan sp = o1d::strip::plan_strip(N, C, H, W, K, sign, 0, va);
     if (sp.ok) return hip_status(fn, o1d::launch_gather_strip((o1d::Dtype)dt, sp, in, w, theta, out, s));
   }
   const o1d::line::LinePlan lp = line_plan(N, C, H, W, K, sign, 0, va);
@@ -147,8 +160,12 @@ o1d_status_t o1d_bwd_weight(const void* x, const void* dy, const float* theta_de
       (need > 0 && (overlaps(workspace, need, x, tbytes) || overlaps(workspace, need, dy, tbytes) ||
                     overlaps(workspace, need, dw, dwbytes))))
     return fail(O1D_ERR_INVALID, "%s: dw or workspace overlaps an input", fn);
-  const o1d::line::LinePlan lp =
-      line_plan(N, C, H, W, K, 1, 1, vec_aligned(x, dtype) && vec_aligned(dy, dtype));
+  const bool va = vec_aligned(x, dtype) && vec_aligned(dy, dtype);
+  const o1d::strip::Plan sp = strip_wgrad_plan(N, C, H, W, K, va);
+  if (sp.ok)
+    return hip_status(fn, o1d::launch_wgrad_strip((o1d::Dtype)dtype, sp, x, dy, theta_deg, dw,
+                                                  static_cast<float*>(workspace), s));
+  const o1d::line::LinePlan lp = line_plan(N, C, H, W, K, 1, 1, va);
   if (lp.ok)
     return hip_status(fn, o1d::launch_wgrad_line((o1d::Dtype)dtype, lp, x, dy, theta_deg, dw,
                                                  static_cast<float*>(workspace), s));

@@ -1,5 +1,5 @@
-// Host-side plan of the strip kernels: the forward pass and the input
-// gradient of the oriented 1D depthwise convolution for K <= 63 and planes
+// Host-side plan of the strip kernels: forward pass, input gradient and
+// weight gradient of the oriented 1D depthwise convolution for K <= 63 and planes
 // whose haloed tile fits in LDS.  The plan depends only on (N, C, H, W, K):
 // angles stay on the device and every workgroup derives its channel's line
 // itself, so the plan covers both staging frames (the plane and its
@@ -115,10 +115,12 @@ struct Plan {
   bool ok = false;
 };
 
+// kind: 0 = gather (forward / input gradient), 1 = weight gradient.
 // vec_ok: tensors aligned for 4-element vector accesses.
-inline Plan plan_strip(int N, int C, int H, int W, int K, int sign, bool vec_ok) {
+inline Plan plan_strip(int N, int C, int H, int W, int K, int sign, int kind, bool vec_ok) {
   Plan pl;
   if (K < 1 || K > kMaxTaps || N < 1 || C < 1 || H < 1 || W < 1) return pl;
+  if (kind == 1 && K > 32) return pl;  // see launch_wgrad_strip
   if (W % 4 != 0 || !vec_ok) return pl;
   const int M = H > W ? H : W;
   const int halo = (K / 2) < (M - 1) ? (K / 2) : (M - 1);
@@ -154,7 +156,8 @@ inline Plan plan_strip(int N, int C, int H, int W, int K, int sign, bool vec_ok)
   if (G * per_plane_slots > max_slots) G = max_slots / per_plane_slots;
   if (G < 1) return pl;
   const int trash = 64 + 3 * S + 4;  // a word per lane plus the reach of a transposed vector write
-  auto lds_for = [&](int g) { return ((size_t)kProgWords + (size_t)g * p.PS + (size_t)trash) * 4; };
+  const int red = kind == 1 ? kWaves * 64 : 0;  // weight gradient: per-wave cell sums
+  auto lds_for = [&](int g) { return ((size_t)kProgWords + (size_t)g * p.PS + (size_t)red + (size_t)trash) * 4; };
   while (G > 1 && lds_for(G) > kLdsBudget) --G;
   if (lds_for(G) > kMaxLdsBytes) return pl;
   // buffer resources cover a group in bytes (float32 at most), below 2^31
@@ -162,12 +165,13 @@ inline Plan plan_strip(int N, int C, int H, int W, int K, int sign, bool vec_ok)
   if ((long long)(G + 1) * C * HW * 4 >= (1ll << 31)) return pl;
   p.G = G;
   p.nq = G * per_plane_slots;
-  p.trash = kProgWords + G * p.PS;
-  // images per workgroup: a default from the LDS rule; the launcher refits
-  // it to the kernel's residency
+  p.trash = kProgWords + G * p.PS + red;
+  // images per workgroup: from the LDS rule and about two waves per SIMD;
+  // the gather launcher refits it to the kernel's residency, the weight
+  // gradient keeps it (its workspace size depends on it)
   const size_t lds = lds_for(G);
   int per_cu = lds_resident(lds);
-  if (per_cu > 6) per_cu = 6;
+  if (per_cu > 4) per_cu = 4;
   const int npw = fit_npw(N, C, G, 256LL * (per_cu < 1 ? 1 : per_cu));
   p.npw = npw;
   pl.S = S;
@@ -189,6 +193,22 @@ O1D_STRIP_DECL(launch_gather_strip_f32_k64)
 O1D_STRIP_DECL(launch_gather_strip_bf16_k32)
 O1D_STRIP_DECL(launch_gather_strip_bf16_k64)
 #undef O1D_STRIP_DECL
+
+#define O1D_STRIP_WDECL(NAME)                                                                                    \
+  hipError_t NAME(const strip::Plan& pl, const void* x, const void* dy, const float* theta, void* dw, float* partial, \
+                  hipStream_t stream);
+O1D_STRIP_WDECL(launch_wgrad_strip_f32_k32)
+O1D_STRIP_WDECL(launch_wgrad_strip_bf16_k32)
+#undef O1D_STRIP_WDECL
+
+// Weight gradient: walks of up to 32 cells only (K <= 32; the per-cell
+// accumulators of longer walks do not fit in registers next to the window).
+inline hipError_t launch_wgrad_strip(Dtype dt, const strip::Plan& pl, const void* x, const void* dy,
+                                     const float* theta, void* dw, float* partial, hipStream_t stream) {
+  if (pl.KB != 32) return hipErrorInvalidValue;
+  return dt == Dtype::F32 ? launch_wgrad_strip_f32_k32(pl, x, dy, theta, dw, partial, stream)
+                          : launch_wgrad_strip_bf16_k32(pl, x, dy, theta, dw, partial, stream);
+}
 
 inline hipError_t launch_gather_strip(Dtype dt, const strip::Plan& pl, const void* in, const void* w,
                                       const float* theta, void* out, hipStream_t stream) {

@@ -1,5 +1,5 @@
-// Device code of the strip kernels (included by the per-storage-type
-// translation units o1d_strip_gather_{f32,bf16}.hip).
+// Device code of the strip kernels (included by the translation units
+// o1d_strip_{gather,wgrad}_{f32,bf16}_k{32,64}.hip).
 //
 // Strip kernels: forward pass and input gradient of the oriented 1D
 // depthwise convolution (Eq. 1: y[p,q] = sum_k w_k x[p + dh_k, q + dw_k],
@@ -249,6 +249,58 @@ struct GatherWalk<R, NC, ST, KB, KB> {
                                              float (&)[R + 1][NC], float (&)[R][NC]) {}
 };
 
+// One cell of the weight-gradient walk: the same window step, then the
+// cell's dot product of the lane's dy block with the window (two partial
+// sums) added to the cell's accumulator.
+template <int R, int NC, int ST, int C, int KB>
+__device__ __forceinline__ void wgrad_cell(float (&sl)[R + 1][NC], uint32_t& base, uint32_t lb, uint32_t vrb,
+                                           uint32_t bits, const float (&dv)[R][NC], float (&acc)[KB]) {
+  constexpr bool kLast = C + 1 == KB;
+  if constexpr (R == kRv && NC == kNv) {
+    if constexpr (kLast)
+      cell_asm_28x1_last<ST, C>(sl, base, lb, vrb, bits);
+    else
+      cell_asm_28x1<ST, C>(sl, base, lb, vrb, bits);
+  } else {
+    static_assert(R == kRd && NC == kNd, "strip shape without a generated window step");
+    if constexpr (kLast)
+      cell_asm_7x4_last<ST, C>(sl, base, lb, vrb, bits);
+    else
+      cell_asm_7x4<ST, C>(sl, base, lb, vrb, bits);
+  }
+  float t0 = 0.f, t1 = 0.f;
+#pragma unroll
+  for (int i = 0; i < R; ++i)
+#pragma unroll
+    for (int k = 0; k < NC; ++k) {
+      if (((i * NC + k) & 1) == 0)
+        t0 = fmaf(dv[i][k], sl[(C + i) % (R + 1)][k], t0);
+      else
+        t1 = fmaf(dv[i][k], sl[(C + i) % (R + 1)][k], t1);
+    }
+  acc[C] += t0 + t1;
+}
+
+// acc[c] += sum over the block of dy * x[cell c + output]: the walk of one
+// block over cells C .. ncells - 1 (the weight gradient of Eq. 1).
+template <int R, int NC, int ST, int C, int KB>
+struct WgradWalk {
+  static __device__ __forceinline__ void run(int n, uint32_t& base, uint32_t lb, uint32_t vrb, uint32_t bits_lo,
+                                             uint32_t bits_hi, float (&sl)[R + 1][NC], const float (&dv)[R][NC],
+                                             float (&acc)[KB]) {
+    int nn = n;
+    asm volatile("" : "+s"(nn));
+    if (C >= nn) return;
+    wgrad_cell<R, NC, ST, C, KB>(sl, base, lb, vrb, C < 32 ? bits_lo : bits_hi, dv, acc);
+    WgradWalk<R, NC, ST, C + 1, KB>::run(n, base, lb, vrb, bits_lo, bits_hi, sl, dv, acc);
+  }
+};
+template <int R, int NC, int ST, int KB>
+struct WgradWalk<R, NC, ST, KB, KB> {
+  static __device__ __forceinline__ void run(int, uint32_t&, uint32_t, uint32_t, uint32_t, uint32_t,
+                                             float (&)[R + 1][NC], const float (&)[R][NC], float (&)[KB]) {}
+};
+
 // ---------------------------------------------------------------- staging
 
 // Staging of a plane group through registers.  Every lane moves 4
@@ -385,15 +437,20 @@ struct Chan {
   uint32_t bits_lo, bits_hi, vrb, vw;
 };
 
-// The group loop of one workgroup for the channel's strip shape (R, NC, SD).
-template <typename T, int S, int KB, int R, int NC, int SD>
-__device__ __forceinline__ void gather_groups(const Params& P, const Chan& ch, float* smem, const T* inc, T* outc,
-                                              int n_begin, int n_end, Stage<T>& stg, uint32_t (&pre)[Stage<T>::kWords]) {
-  constexpr int ST = S + SD;
+// A lane's block of the group: plane g, frame rows b0 .. b0 + R - 1, strip
+// columns j0 .. j0 + NC - 1 (strip column j holds the outputs (b0 + i,
+// j + SD i)), and the LDS address of its first output in the tile.  Lanes
+// without a task point at a real block (their reads stay in the tile).
+struct Block {
+  int g, b0, j0;
+  bool task;  // the lane has a block
+  bool full;  // the block lies inside the plane
+  uint32_t lb;
+};
+
+template <int S, int R, int NC, int SD>
+__device__ __forceinline__ Block block_of(const Params& P, const Chan& ch, const float* tiles) {
   const Shape sh = shape_of(ch.Hs, ch.Ws, SD);
-  const size_t img = (size_t)P.C * P.H * P.W;
-  float* tiles = smem + kProgWords;
-  // this lane's block: plane g of the group, rows b0 .. b0 + R - 1, strip columns j0 .. j0 + NC - 1
   const int t = threadIdx.x;
   int g = t / sh.ppt;
   const int r = t - g * sh.ppt;
@@ -406,15 +463,28 @@ __device__ __forceinline__ void gather_groups(const Params& P, const Chan& ch, f
     cg = 8 * bqi + (r & 7);
     band = 4 * bbi + ((r >> 3) & 3);
   }
-  const bool task = g < P.G && band < sh.nb && cg < sh.ncg;
-  if (!task) g = 0;
-  const int b0 = task ? band * R : 0;
-  const int j0 = task ? sh.jlo + cg * NC : sh.jlo;
-  const uint32_t lb = lds_addr(tiles + g * P.PS + kGuard + (P.halo + b0) * S + P.mc + j0);
-  // outputs outside the plane are written as zeros (into the tile's margins)
-  bool full = b0 + R <= ch.Hs;
-  const int cmin = j0 + (SD < 0 ? -(R - 1) : 0), cmax = j0 + NC - 1 + (SD > 0 ? R - 1 : 0);
-  full = full && cmin >= 0 && cmax < ch.Ws;
+  Block bk;
+  bk.task = g < P.G && band < sh.nb && cg < sh.ncg;
+  bk.g = bk.task ? g : 0;
+  bk.b0 = bk.task ? band * R : 0;
+  bk.j0 = bk.task ? sh.jlo + cg * NC : sh.jlo;
+  bk.lb = lds_addr(tiles + bk.g * P.PS + kGuard + (P.halo + bk.b0) * S + P.mc + bk.j0);
+  const int cmin = bk.j0 + (SD < 0 ? -(R - 1) : 0), cmax = bk.j0 + NC - 1 + (SD > 0 ? R - 1 : 0);
+  bk.full = bk.b0 + R <= ch.Hs && cmin >= 0 && cmax < ch.Ws;
+  return bk;
+}
+
+// The group loop of one workgroup for the channel's strip shape (R, NC, SD).
+template <typename T, int S, int KB, int R, int NC, int SD>
+__device__ __forceinline__ void gather_groups(const Params& P, const Chan& ch, float* smem, const T* inc, T* outc,
+                                              int n_begin, int n_end, Stage<T>& stg, uint32_t (&pre)[Stage<T>::kWords]) {
+  constexpr int ST = S + SD;
+  const size_t img = (size_t)P.C * P.H * P.W;
+  float* tiles = smem + kProgWords;
+  const Block bk = block_of<S, R, NC, SD>(P, ch, tiles);
+  const int g = bk.g, b0 = bk.b0, j0 = bk.j0;
+  const bool task = bk.task, full = bk.full;
+  const uint32_t lb = bk.lb;
 
   for (int n0 = n_begin; n0 < n_end; n0 += P.G) {
     const int ng = min(P.G, n_end - n0);
@@ -506,6 +576,125 @@ __global__ __launch_bounds__(kThreads) void strip_gather(Params P, const T* __re
     gather_groups<T, S, KB, kRd, kNd, -1>(P, ch, smem, inc, outc, n_begin, n_end, stg, pre);
 }
 
+// ---------------------------------------------------------------- weight gradient
+
+// The group loop of the weight gradient.  Per group the tile first holds dy
+// (every lane copies the dy of its block into registers; the tile's zero
+// margins give zeros outside the plane), then x, which the lanes walk.  The
+// next group's x is prefetched during the walk; dy is loaded at the start
+// of its group (one prefetch buffer keeps the registers for the walk).
+template <typename T, int S, int KB, int R, int NC, int SD>
+__device__ __forceinline__ void wgrad_groups(const Params& P, const Chan& ch, float* smem, const T* xc, const T* dc,
+                                             int n_begin, int n_end, Stage<T>& stg,
+                                             uint32_t (&xpre)[Stage<T>::kWords], float (&acc)[KB]) {
+  constexpr int ST = S + SD;
+  const size_t img = (size_t)P.C * P.H * P.W;
+  float* tiles = smem + kProgWords;
+  const Block bk = block_of<S, R, NC, SD>(P, ch, tiles);
+  for (int n0 = n_begin; n0 < n_end; n0 += P.G) {
+    {
+      uint32_t dpre[Stage<T>::kWords];
+      stg.load(P, dc + (size_t)n0 * img, min(P.G, n_end - n0), dpre);
+      stg.store_lds(P, S, ch.tr != 0, dpre);
+    }
+    __syncthreads();  // dy of the group is in the tile
+    float dv[R][NC];
+#pragma unroll
+    for (int i = 0; i < R; ++i)
+#pragma unroll
+      for (int k = 0; k < NC; ++k) dv[i][k] = bk.task ? lds_load(bk.lb + 4 * (i * ST + k)) : 0.f;
+    __syncthreads();  // every lane has its dy
+    stg.store_lds(P, S, ch.tr != 0, xpre);
+    __syncthreads();  // x of the group is in the tile
+    // the next group's x (past the end: an empty range, see gather_groups)
+    const int nn = max(0, min(P.G, n_end - n0 - P.G));
+    stg.load(P, xc + (size_t)(nn > 0 ? n0 + P.G : n_begin) * img, nn, xpre);
+    float sl[R + 1][NC];
+    uint32_t base = bk.lb;
+    WgradWalk<R, NC, ST, 0, KB>::run(ch.ncells, base, bk.lb, ch.vrb, ch.bits_lo, ch.bits_hi, sl, dv, acc);
+    asm volatile("s_waitcnt lgkmcnt(0)" ::: "memory");
+    __syncthreads();  // the tile is free
+  }
+}
+
+// Weight gradient: partial[(blockIdx.x * C + c) * K + k] = sum over the
+// workgroup's images of dy * x[tap k + output] (Eq. 1 differentiated in w),
+// reduced over lanes and waves in a fixed order (no atomics).
+template <typename T, int S, int KB>
+__global__ __launch_bounds__(kThreads) void strip_wgrad(Params P, const T* __restrict__ x, const T* __restrict__ dy,
+                                                        const float* __restrict__ theta, float* __restrict__ partial) {
+  extern __shared__ float smem[];
+  Prog* pg = reinterpret_cast<Prog*>(smem);
+  float* tiles = smem + kProgWords;
+  float* red = smem + P.trash - kWaves * 64;  // per-wave cell sums, just below the trash area
+  const int c = blockIdx.y;
+  const int tid = threadIdx.x, lane = tid & 63;
+  const int wave = __builtin_amdgcn_readfirstlane(tid >> 6);
+  const size_t HW = (size_t)P.H * P.W;
+  const size_t img = (size_t)P.C * HW;
+  const int n_begin = blockIdx.x * P.npw;
+  const int n_end = min(P.N, n_begin + P.npw);
+  const T* xc = x + (size_t)c * HW;
+  const T* dc = dy + (size_t)c * HW;
+
+  Stage<T> stg;
+  stg.init_global(P);
+  uint32_t xpre[Stage<T>::kWords];
+  stg.load(P, xc + (size_t)n_begin * img, min(P.G, n_end - n_begin), xpre);
+  for (int i = tid; i < P.G * P.PS; i += kThreads) tiles[i] = 0.f;  // margins and guards stay zero
+  if (wave == 0) build_prog<T>(pg, static_cast<const T*>(nullptr), theta[c], c, P.K, 1, P.H, P.W, S);
+  __syncthreads();
+  Chan ch;
+  ch.tr = __builtin_amdgcn_readfirstlane(pg->tr);
+  ch.s = __builtin_amdgcn_readfirstlane(pg->s);
+  ch.ncells = min(__builtin_amdgcn_readfirstlane(pg->ncells), KB);
+  ch.bits_lo = __builtin_amdgcn_readfirstlane(pg->brk[0]);
+  ch.bits_hi = __builtin_amdgcn_readfirstlane(pg->brk[1]);
+  ch.vrb = (uint32_t)pg->rbase[lane];
+  ch.vw = 0u;
+  ch.Hs = ch.tr ? P.W : P.H;
+  ch.Ws = ch.tr ? P.H : P.W;
+  stg.init_lds(P, S, ch.tr != 0, lds_addr(tiles), lds_addr(smem + P.trash));
+  float acc[KB];
+#pragma unroll
+  for (int i = 0; i < KB; ++i) acc[i] = 0.f;
+  if (ch.s == 0)
+    wgrad_groups<T, S, KB, kRv, kNv, 0>(P, ch, smem, xc, dc, n_begin, n_end, stg, xpre, acc);
+  else if (ch.s > 0)
+    wgrad_groups<T, S, KB, kRd, kNd, 1>(P, ch, smem, xc, dc, n_begin, n_end, stg, xpre, acc);
+  else
+    wgrad_groups<T, S, KB, kRd, kNd, -1>(P, ch, smem, xc, dc, n_begin, n_end, stg, xpre, acc);
+  // lanes -> per-wave cell sums -> per-tap partial of this workgroup, in a fixed order
+#pragma unroll
+  for (int ci = 0; ci < KB; ++ci) {
+    if (ci < ch.ncells) {
+      float v = acc[ci];
+#pragma unroll
+      for (int m = 32; m >= 1; m >>= 1) v += __shfl_xor(v, m, 64);
+      if (lane == 0) red[wave * 64 + ci] = v;
+    }
+  }
+  __syncthreads();
+  for (int k = tid; k < P.K; k += kThreads) {
+    const int ci = pg->tap_cell[k];
+    float v = 0.f;
+    if (ci >= 0 && ci < KB)
+      for (int w = 0; w < kWaves; ++w) v += red[w * 64 + ci];
+    partial[((size_t)blockIdx.x * P.C + c) * (size_t)P.K + k] = pg->finite ? v : __builtin_nanf("");
+  }
+}
+
+// dw[i] = sum over the partial rows, in a fixed order.
+template <typename T>
+__global__ __launch_bounds__(256) void strip_wgrad_reduce(const float* __restrict__ partial, T* __restrict__ dw,
+                                                          int CK, int parts) {
+  const int i = blockIdx.x * blockDim.x + threadIdx.x;
+  if (i >= CK) return;
+  float s = 0.f;
+  for (int j = 0; j < parts; ++j) s += partial[(size_t)j * CK + i];
+  dw[i] = from_f32<T>(s);
+}
+
 // ---------------------------------------------------------------- launch
 
 // Fits the grid to `per_cu` resident workgroups on every CU of the device.
@@ -568,6 +757,32 @@ hipError_t gather_launch(const Plan& plan, const void* in, const void* w, const 
   hipLaunchKernelGGL((strip_gather<T, S, KB>), dim3((unsigned)pl.blocks_n, (unsigned)pl.p.C, 1), dim3(kThreads),
                      pl.lds_bytes, stream, pl.p, static_cast<const T*>(in), static_cast<const T*>(w), theta,
                      static_cast<T*>(out));
+  return hipGetLastError();
+}
+
+template <typename T, int S, int KB>
+hipError_t wgrad_launch(const Plan& pl, const void* x, const void* dy, const float* theta, float* partial,
+                        hipStream_t stream) {
+  hipError_t e = hipFuncSetAttribute(reinterpret_cast<const void*>(strip_wgrad<T, S, KB>),
+                                     hipFuncAttributeMaxDynamicSharedMemorySize, (int)kMaxLdsBytes);
+  if (e != hipSuccess) return e;
+  hipLaunchKernelGGL((strip_wgrad<T, S, KB>), dim3((unsigned)pl.blocks_n, (unsigned)pl.p.C, 1), dim3(kThreads),
+                     pl.lds_bytes, stream, pl.p, static_cast<const T*>(x), static_cast<const T*>(dy), theta, partial);
+  return hipGetLastError();
+}
+
+template <typename T, int KB>
+hipError_t wgrad_t(const Plan& pl, const void* x, const void* dy, const float* theta, void* dw, float* partial,
+                   hipStream_t stream) {
+  hipError_t e = hipErrorInvalidValue;
+#define O1D_CASE(SV) \
+  if (pl.S == SV) e = wgrad_launch<T, SV, KB>(pl, x, dy, theta, partial, stream);
+  O1D_STRIP_STRIDES(O1D_CASE)
+#undef O1D_CASE
+  if (e != hipSuccess) return e;
+  const int CK = pl.p.C * pl.p.K;
+  hipLaunchKernelGGL(strip_wgrad_reduce<T>, dim3((unsigned)((CK + 255) / 256)), dim3(256), 0, stream, partial,
+                     static_cast<T*>(dw), CK, pl.blocks_n);
   return hipGetLastError();
 }
 
