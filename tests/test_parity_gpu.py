@@ -125,6 +125,33 @@ def test_edges(case, dtype):
     run_case(wl, label=f"edge {case} {dtype}")
 
 
+# Shapes the strip kernels take (W % 4 == 0, aligned tensors): non-square
+# planes in both staging frames, bands that do not fill the last strip,
+# groups of several planes with a partial last group, walks of up to 64
+# cells, and the line-kernel fallback next to them.
+EDGE_STRIP = [
+    # (N, C, H, W, K, theta mode)
+    (3, 5, 20, 44, 31, "uniform"),     # H != W, ragged bands, several planes per group
+    (5, 3, 44, 20, 15, "discrete8"),   # tall plane, N not a multiple of the group
+    (2, 4, 56, 56, 1, "uniform"),      # one cell
+    (2, 4, 56, 56, 3, "discrete8"),
+    (2, 3, 36, 48, 45, "uniform"),     # walks of up to 64 cells (weight gradient: line kernel)
+    (7, 2, 12, 16, 31, "uniform"),     # K larger than the plane, many planes per group
+    (3, 2, 96, 8, 7, "uniform"),       # tall and narrow
+    (2, 3, 8, 100, 7, "uniform"),      # short and wide
+    (1, 2, 64, 64, 31, "uniform"),     # more tasks than a workgroup: line kernels
+    (9, 4, 28, 28, 31, "groups:8"),    # the paper's D equal groups
+]
+
+
+@pytest.mark.parametrize("case", EDGE_STRIP, ids=lambda c: "x".join(map(str, c[:5])) + "-" + c[5])
+@pytest.mark.parametrize("dtype", ["f32", "bf16"])
+def test_strip_edges(case, dtype):
+    N, C, H, W, K, mode = case
+    wl = synth.Workload("strip-edge", N, C, H, W, K, dtype, mode, "fwd+bwd", 13)
+    run_case(wl, label=f"strip edge {case} {dtype}")
+
+
 def test_angles_outside_zero_180():
     wl = synth.Workload("angles", 2, 12, 23, 29, 15, "f32", "uniform", "fwd+bwd", 12)
     d = synth.make_inputs(wl)
