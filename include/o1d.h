@@ -41,7 +41,7 @@
  * any, surface at the caller's next synchronisation.
  *
  * Empty tensors: a zero N, C, H or W is valid.  Nothing is launched, except
- * that o1d_bwd_weight with C > 0 writes zeros to dw (an empty sum).
+ * that o1d_bwd_weight and o1d_bwd with C > 0 write zeros to dw (an empty sum).
  */
 #ifndef O1D_H_
 #define O1D_H_
@@ -89,7 +89,23 @@ o1d_status_t o1d_bwd_weight(const void* x, const void* dy, const float* theta_de
                             int N, int C, int H, int W, int K, o1d_dtype_t dtype,
                             void* workspace, size_t workspace_bytes, void* stream);
 
-/* Workspace size in bytes that o1d_bwd_weight needs for these sizes. */
+/* Both gradients of Eq. (1) in one call: dx as o1d_bwd_input computes it
+ * (from dy and w) and dw as o1d_bwd_weight computes it (from x and dy).
+ * Where the sizes allow (K <= 31, W a multiple of 4, x, dy and dx aligned
+ * to 16 bytes for O1D_F32 or 8 bytes for O1D_BF16, planes whose zero-padded
+ * tile fits in LDS) one kernel reads x and dy once and produces both; otherwise
+ * the kernels of the two separate entry points run in turn.  The results
+ * equal those of the separate calls up to the order of floating-point
+ * additions and are bitwise reproducible for the same inputs.  dx and dw
+ * are overwritten.  `workspace` follows the rules of o1d_bwd_weight and
+ * needs o1d_bwd_weight_workspace_bytes(...) bytes.  No output may overlap
+ * an input, the other output or the workspace.  With N, H or W zero and
+ * C > 0, dw is set to zeros. */
+o1d_status_t o1d_bwd(const void* x, const void* dy, const void* w, const float* theta_deg, void* dx, void* dw,
+                     int N, int C, int H, int W, int K, o1d_dtype_t dtype,
+                     void* workspace, size_t workspace_bytes, void* stream);
+
+/* Workspace size in bytes that o1d_bwd_weight (and o1d_bwd) needs for these sizes. */
 size_t o1d_bwd_weight_workspace_bytes(int N, int C, int H, int W, int K, o1d_dtype_t dtype);
 
 /* Static description of a status code. */

@@ -21,6 +21,7 @@ SIGNATURES = {
     "o1d_fwd": (_i, [_vp, _vp, _vp, _vp, _i, _i, _i, _i, _i, _i, _vp]),
     "o1d_bwd_input": (_i, [_vp, _vp, _vp, _vp, _i, _i, _i, _i, _i, _i, _vp]),
     "o1d_bwd_weight": (_i, [_vp, _vp, _vp, _vp, _i, _i, _i, _i, _i, _i, _vp, _sz, _vp]),
+    "o1d_bwd": (_i, [_vp, _vp, _vp, _vp, _vp, _vp, _i, _i, _i, _i, _i, _i, _vp, _sz, _vp]),
     "o1d_bwd_weight_workspace_bytes": (_sz, [_i, _i, _i, _i, _i, _i]),
     "o1d_status_str": (ctypes.c_char_p, [_i]),
     "o1d_last_error": (ctypes.c_char_p, []),

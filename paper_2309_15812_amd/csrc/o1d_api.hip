@@ -120,6 +120,23 @@ o1d_status_t gather_entry(const char* fn, const void* in, const void* w, const f
   return hip_status(fn, o1d::launch_gather((o1d::Dtype)dt, in, w, theta, out, N, C, H, W, K, sign, s));
 }
 
+// Weight gradient after validation: the strip kernel, else a line kernel,
+// else the tiled kernels (the workspace covers all three, see above).
+o1d_status_t wgrad_dispatch(const char* fn, const void* x, const void* dy, const float* theta, void* dw, int N, int C,
+                            int H, int W, int K, o1d_dtype_t dt, void* workspace, hipStream_t s) {
+  const bool va = vec_aligned(x, dt) && vec_aligned(dy, dt);
+  const o1d::strip::Plan sp = strip_wgrad_plan(N, C, H, W, K, va);
+  if (sp.ok)
+    return hip_status(fn, o1d::launch_wgrad_strip((o1d::Dtype)dt, sp, x, dy, theta, dw,
+                                                  static_cast<float*>(workspace), s));
+  const o1d::line::LinePlan lp = line_plan(N, C, H, W, K, 1, 1, va);
+  if (lp.ok)
+    return hip_status(fn, o1d::launch_wgrad_line((o1d::Dtype)dt, lp, x, dy, theta, dw,
+                                                 static_cast<float*>(workspace), s));
+  return hip_status(fn, o1d::launch_wgrad((o1d::Dtype)dt, x, dy, theta, dw, static_cast<float*>(workspace), N, C, H,
+                                          W, K, s));
+}
+
 }  // namespace
 
 extern "C" {
@@ -160,17 +177,46 @@ o1d_status_t o1d_bwd_weight(const void* x, const void* dy, const float* theta_de
       (need > 0 && (overlaps(workspace, need, x, tbytes) || overlaps(workspace, need, dy, tbytes) ||
                     overlaps(workspace, need, dw, dwbytes))))
     return fail(O1D_ERR_INVALID, "%s: dw or workspace overlaps an input", fn);
-  const bool va = vec_aligned(x, dtype) && vec_aligned(dy, dtype);
-  const o1d::strip::Plan sp = strip_wgrad_plan(N, C, H, W, K, va);
-  if (sp.ok)
-    return hip_status(fn, o1d::launch_wgrad_strip((o1d::Dtype)dtype, sp, x, dy, theta_deg, dw,
+  return wgrad_dispatch(fn, x, dy, theta_deg, dw, N, C, H, W, K, dtype, workspace, s);
+}
+
+o1d_status_t o1d_bwd(const void* x, const void* dy, const void* w, const float* theta_deg, void* dx, void* dw, int N,
+                     int C, int H, int W, int K, o1d_dtype_t dtype, void* workspace, size_t workspace_bytes,
+                     void* stream) {
+  const char* fn = "o1d_bwd";
+  o1d_status_t st = check_sizes(fn, N, C, H, W, K, dtype);
+  if (st != O1D_OK) return st;
+  if (C == 0) return ok();
+  if (!dw) return fail(O1D_ERR_INVALID, "%s: NULL dw pointer", fn);
+  hipStream_t s = static_cast<hipStream_t>(stream);
+  const size_t elems = (size_t)N * C * H * W;
+  (void)hipGetLastError();
+  if (elems == 0) return hip_status(fn, o1d::launch_zero((o1d::Dtype)dtype, dw, (size_t)C * K, s));
+  if (!x || !dy || !w || !theta_deg || !dx) return fail(O1D_ERR_INVALID, "%s: NULL tensor pointer", fn);
+  const size_t need = o1d_bwd_weight_workspace_bytes(N, C, H, W, K, dtype);
+  if (workspace_bytes < need || (need > 0 && !workspace))
+    return fail(O1D_ERR_WORKSPACE, "%s: workspace of %zu bytes given, %zu needed", fn, workspace_bytes, need);
+  const size_t wbytes = (size_t)C * K * elem_size(dtype), tbytes = elems * elem_size(dtype);
+  if (overlaps(dx, tbytes, x, tbytes) || overlaps(dx, tbytes, dy, tbytes) || overlaps(dx, tbytes, w, wbytes))
+    return fail(O1D_ERR_INVALID, "%s: dx overlaps an input", fn);
+  if (overlaps(dw, wbytes, x, tbytes) || overlaps(dw, wbytes, dy, tbytes) || overlaps(dw, wbytes, w, wbytes) ||
+      overlaps(dw, wbytes, dx, tbytes))
+    return fail(O1D_ERR_INVALID, "%s: dw overlaps an input or dx", fn);
+  if (need > 0 && (overlaps(workspace, need, x, tbytes) || overlaps(workspace, need, dy, tbytes) ||
+                   overlaps(workspace, need, w, wbytes) || overlaps(workspace, need, dx, tbytes) ||
+                   overlaps(workspace, need, dw, wbytes)))
+    return fail(O1D_ERR_INVALID, "%s: workspace overlaps a tensor", fn);
+  const bool va = vec_aligned(x, dtype) && vec_aligned(dy, dtype) && vec_aligned(dx, dtype);
+  if (line_allowed()) {
+    // the weight gradient's plan (hence its workspace) with mirrored offsets
+    o1d::strip::Plan sp = o1d::strip::plan_strip(N, C, H, W, K, -1, 1, va);
+    if (sp.ok)
+      return hip_status(fn, o1d::launch_bwd_strip((o1d::Dtype)dtype, sp, x, dy, w, theta_deg, dx, dw,
                                                   static_cast<float*>(workspace), s));
-  const o1d::line::LinePlan lp = line_plan(N, C, H, W, K, 1, 1, va);
-  if (lp.ok)
-    return hip_status(fn, o1d::launch_wgrad_line((o1d::Dtype)dtype, lp, x, dy, theta_deg, dw,
-                                                 static_cast<float*>(workspace), s));
-  return hip_status(fn, o1d::launch_wgrad((o1d::Dtype)dtype, x, dy, theta_deg, dw, static_cast<float*>(workspace), N,
-                                          C, H, W, K, s));
+  }
+  st = gather_entry(fn, dy, w, theta_deg, dx, N, C, H, W, K, dtype, stream, -1);
+  if (st != O1D_OK) return st;
+  return wgrad_dispatch(fn, x, dy, theta_deg, dw, N, C, H, W, K, dtype, workspace, s);
 }
 
 const char* o1d_status_str(o1d_status_t status) {

@@ -201,6 +201,22 @@ O1D_STRIP_WDECL(launch_wgrad_strip_f32_k32)
 O1D_STRIP_WDECL(launch_wgrad_strip_bf16_k32)
 #undef O1D_STRIP_WDECL
 
+#define O1D_STRIP_BDECL(NAME)                                                                                   \
+  hipError_t NAME(const strip::Plan& pl, const void* x, const void* dy, const void* w, const float* theta, void* dx, \
+                  void* dw, float* partial, hipStream_t stream);
+O1D_STRIP_BDECL(launch_bwd_strip_f32_k32)
+O1D_STRIP_BDECL(launch_bwd_strip_bf16_k32)
+#undef O1D_STRIP_BDECL
+
+// Fused backward (input and weight gradients in one pass): the weight
+// gradient's plan with mirrored offsets (sign -1), walks of up to 32 cells.
+inline hipError_t launch_bwd_strip(Dtype dt, const strip::Plan& pl, const void* x, const void* dy, const void* w,
+                                   const float* theta, void* dx, void* dw, float* partial, hipStream_t stream) {
+  if (pl.KB != 32 || pl.p.sign != -1) return hipErrorInvalidValue;
+  return dt == Dtype::F32 ? launch_bwd_strip_f32_k32(pl, x, dy, w, theta, dx, dw, partial, stream)
+                          : launch_bwd_strip_bf16_k32(pl, x, dy, w, theta, dx, dw, partial, stream);
+}
+
 // Weight gradient: walks of up to 32 cells only (K <= 32; the per-cell
 // accumulators of longer walks do not fit in registers next to the window).
 inline hipError_t launch_wgrad_strip(Dtype dt, const strip::Plan& pl, const void* x, const void* dy,

@@ -1,5 +1,5 @@
 // Device code of the strip kernels (included by the translation units
-// o1d_strip_{gather,wgrad}_{f32,bf16}_k{32,64}.hip).
+// o1d_strip_{gather,wgrad,bwd}_{f32,bf16}_k{32,64}.hip).
 //
 // Strip kernels: forward pass and input gradient of the oriented 1D
 // depthwise convolution (Eq. 1: y[p,q] = sum_k w_k x[p + dh_k, q + dw_k],
@@ -201,11 +201,12 @@ __device__ __forceinline__ void lds_store(uint32_t a, float v) {
   *(__attribute__((address_space(3))) float*)(uintptr_t)a = v;
 }
 
-// One cell of the gather walk: the window step (generated inline assembly)
-// and the cell's R * NC multiplies.
+// The window step of cell C (generated inline assembly): a run's first
+// cell reloads all R rows, every cell but the walk's last reads the next
+// cell's new row.
 template <int R, int NC, int ST, int C, int KB>
-__device__ __forceinline__ void gather_cell(float (&sl)[R + 1][NC], uint32_t& base, uint32_t lb, uint32_t vrb,
-                                            uint32_t bits, uint32_t vw, float (&acc)[R][NC]) {
+__device__ __forceinline__ void window_step(float (&sl)[R + 1][NC], uint32_t& base, uint32_t lb, uint32_t vrb,
+                                            uint32_t bits) {
   constexpr bool kLast = C + 1 == KB;
   if constexpr (R == kRv && NC == kNv) {
     if constexpr (kLast)
@@ -219,6 +220,14 @@ __device__ __forceinline__ void gather_cell(float (&sl)[R + 1][NC], uint32_t& ba
     else
       cell_asm_7x4<ST, C>(sl, base, lb, vrb, bits);
   }
+}
+
+// One cell of the gather walk: the window step and the cell's R * NC
+// multiplies.
+template <int R, int NC, int ST, int C, int KB>
+__device__ __forceinline__ void gather_cell(float (&sl)[R + 1][NC], uint32_t& base, uint32_t lb, uint32_t vrb,
+                                            uint32_t bits, uint32_t vw, float (&acc)[R][NC]) {
+  window_step<R, NC, ST, C, KB>(sl, base, lb, vrb, bits);
   const float wc = __int_as_float(__builtin_amdgcn_readlane((int)vw, C));
 #pragma unroll
   for (int i = 0; i < R; ++i)
@@ -255,19 +264,7 @@ struct GatherWalk<R, NC, ST, KB, KB> {
 template <int R, int NC, int ST, int C, int KB>
 __device__ __forceinline__ void wgrad_cell(float (&sl)[R + 1][NC], uint32_t& base, uint32_t lb, uint32_t vrb,
                                            uint32_t bits, const float (&dv)[R][NC], float (&acc)[KB]) {
-  constexpr bool kLast = C + 1 == KB;
-  if constexpr (R == kRv && NC == kNv) {
-    if constexpr (kLast)
-      cell_asm_28x1_last<ST, C>(sl, base, lb, vrb, bits);
-    else
-      cell_asm_28x1<ST, C>(sl, base, lb, vrb, bits);
-  } else {
-    static_assert(R == kRd && NC == kNd, "strip shape without a generated window step");
-    if constexpr (kLast)
-      cell_asm_7x4_last<ST, C>(sl, base, lb, vrb, bits);
-    else
-      cell_asm_7x4<ST, C>(sl, base, lb, vrb, bits);
-  }
+  window_step<R, NC, ST, C, KB>(sl, base, lb, vrb, bits);
   float t0 = 0.f, t1 = 0.f;
 #pragma unroll
   for (int i = 0; i < R; ++i)
@@ -299,6 +296,51 @@ template <int R, int NC, int ST, int KB>
 struct WgradWalk<R, NC, ST, KB, KB> {
   static __device__ __forceinline__ void run(int, uint32_t&, uint32_t, uint32_t, uint32_t, uint32_t,
                                              float (&)[R + 1][NC], const float (&)[R][NC], float (&)[KB]) {}
+};
+
+// One cell of the fused backward walk over dy with the mirrored program:
+// the window step, then every window value feeds the lane's input-gradient
+// block (times the cell's weight) and the cell's weight-gradient dot
+// product (times the lane's x).  KW bounds the walk (its last cell reads
+// no next row); acc holds KB >= KW cells.
+template <int R, int NC, int ST, int C, int KW, int KB>
+__device__ __forceinline__ void bwd_cell(float (&sl)[R + 1][NC], uint32_t& base, uint32_t lb, uint32_t vrb,
+                                         uint32_t bits, uint32_t vw, const float (&xv)[R][NC], float (&out)[R][NC],
+                                         float (&acc)[KB]) {
+  window_step<R, NC, ST, C, KW>(sl, base, lb, vrb, bits);
+  const float wc = __int_as_float(__builtin_amdgcn_readlane((int)vw, C));
+  float t0 = 0.f, t1 = 0.f;
+#pragma unroll
+  for (int i = 0; i < R; ++i)
+#pragma unroll
+    for (int k = 0; k < NC; ++k) {
+      const float v = sl[(C + i) % (R + 1)][k];
+      out[i][k] = fmaf(wc, v, out[i][k]);
+      if (((i * NC + k) & 1) == 0)
+        t0 = fmaf(xv[i][k], v, t0);
+      else
+        t1 = fmaf(xv[i][k], v, t1);
+    }
+  acc[C] += t0 + t1;
+}
+
+template <int R, int NC, int ST, int C, int KW, int KB>
+struct BwdWalk {
+  static __device__ __forceinline__ void run(int n, uint32_t& base, uint32_t lb, uint32_t vrb, uint32_t bits_lo,
+                                             uint32_t bits_hi, uint32_t vw, float (&sl)[R + 1][NC],
+                                             const float (&xv)[R][NC], float (&out)[R][NC], float (&acc)[KB]) {
+    int nn = n;
+    asm volatile("" : "+s"(nn));
+    if (C >= nn) return;
+    bwd_cell<R, NC, ST, C, KW, KB>(sl, base, lb, vrb, C < 32 ? bits_lo : bits_hi, vw, xv, out, acc);
+    BwdWalk<R, NC, ST, C + 1, KW, KB>::run(n, base, lb, vrb, bits_lo, bits_hi, vw, sl, xv, out, acc);
+  }
+};
+template <int R, int NC, int ST, int KW, int KB>
+struct BwdWalk<R, NC, ST, KW, KW, KB> {
+  static __device__ __forceinline__ void run(int, uint32_t&, uint32_t, uint32_t, uint32_t, uint32_t, uint32_t,
+                                             float (&)[R + 1][NC], const float (&)[R][NC], float (&)[R][NC],
+                                             float (&)[KB]) {}
 };
 
 // ---------------------------------------------------------------- staging
@@ -474,6 +516,27 @@ __device__ __forceinline__ Block block_of(const Params& P, const Chan& ch, const
   return bk;
 }
 
+// Writes a lane's block of outputs into the tile at its own positions,
+// zeros for positions outside the plane (the margins stay zero).
+template <int R, int NC, int ST, int SD>
+__device__ __forceinline__ void put_block(const Block& bk, const Chan& ch, const float (&v)[R][NC]) {
+  if (bk.full) {
+#pragma unroll
+    for (int i = 0; i < R; ++i)
+#pragma unroll
+      for (int k = 0; k < NC; ++k) lds_store(bk.lb + 4 * (i * ST + k), v[i][k]);
+  } else {
+#pragma unroll
+    for (int i = 0; i < R; ++i)
+#pragma unroll
+      for (int k = 0; k < NC; ++k) {
+        const int col = bk.j0 + SD * i + k;
+        const bool in = bk.b0 + i < ch.Hs && col >= 0 && col < ch.Ws;
+        lds_store(bk.lb + 4 * (i * ST + k), in ? v[i][k] : 0.f);
+      }
+  }
+}
+
 // The group loop of one workgroup for the channel's strip shape (R, NC, SD).
 template <typename T, int S, int KB, int R, int NC, int SD>
 __device__ __forceinline__ void gather_groups(const Params& P, const Chan& ch, float* smem, const T* inc, T* outc,
@@ -482,8 +545,8 @@ __device__ __forceinline__ void gather_groups(const Params& P, const Chan& ch, f
   const size_t img = (size_t)P.C * P.H * P.W;
   float* tiles = smem + kProgWords;
   const Block bk = block_of<S, R, NC, SD>(P, ch, tiles);
-  const int g = bk.g, b0 = bk.b0, j0 = bk.j0;
-  const bool task = bk.task, full = bk.full;
+  const int g = bk.g;
+  const bool task = bk.task;
   const uint32_t lb = bk.lb;
 
   for (int n0 = n_begin; n0 < n_end; n0 += P.G) {
@@ -504,23 +567,7 @@ __device__ __forceinline__ void gather_groups(const Params& P, const Chan& ch, f
     // the last cell's read-ahead (of a cell that does not exist) may still be in flight
     asm volatile("s_waitcnt lgkmcnt(0)" ::: "memory");
     __syncthreads();  // every lane has finished reading the tile
-    if (task && g < ng) {
-      if (full) {
-#pragma unroll
-        for (int i = 0; i < R; ++i)
-#pragma unroll
-          for (int k = 0; k < NC; ++k) lds_store(lb + 4 * (i * ST + k), acc[i][k]);
-      } else {
-#pragma unroll
-        for (int i = 0; i < R; ++i)
-#pragma unroll
-          for (int k = 0; k < NC; ++k) {
-            const int col = j0 + SD * i + k;
-            const bool in = b0 + i < ch.Hs && col >= 0 && col < ch.Ws;
-            lds_store(lb + 4 * (i * ST + k), in ? acc[i][k] : 0.f);
-          }
-      }
-    }
+    if (task && g < ng) put_block<R, NC, ST, SD>(bk, ch, acc);
     __syncthreads();  // the group's outputs are in the tile
     float e[Stage<T>::kQ][4];
     stg.read_lds(P, S, ch.tr != 0, e);
@@ -617,6 +664,35 @@ __device__ __forceinline__ void wgrad_groups(const Params& P, const Chan& ch, fl
   }
 }
 
+// partial[(blockIdx.x * C + c) * K + k] = the workgroup's sum for tap k:
+// lanes -> per-wave cell sums (in `red`, kWaves * 64 floats) -> the cell of
+// every tap, in a fixed order (no atomics).  A channel whose angle is not
+// finite gets NaN.
+template <int KB>
+__device__ __forceinline__ void write_partial(const Params& P, const Prog* pg, float* red, int ncells,
+                                              const float (&acc)[KB], float* __restrict__ partial) {
+  const int c = blockIdx.y;
+  const int tid = threadIdx.x, lane = tid & 63;
+  const int wave = __builtin_amdgcn_readfirstlane(tid >> 6);
+#pragma unroll
+  for (int ci = 0; ci < KB; ++ci) {
+    if (ci < ncells) {
+      float v = acc[ci];
+#pragma unroll
+      for (int m = 32; m >= 1; m >>= 1) v += __shfl_xor(v, m, 64);
+      if (lane == 0) red[wave * 64 + ci] = v;
+    }
+  }
+  __syncthreads();
+  for (int k = tid; k < P.K; k += kThreads) {
+    const int ci = pg->tap_cell[k];
+    float v = 0.f;
+    if (ci >= 0 && ci < KB)
+      for (int w = 0; w < kWaves; ++w) v += red[w * 64 + ci];
+    partial[((size_t)blockIdx.x * P.C + c) * (size_t)P.K + k] = pg->finite ? v : __builtin_nanf("");
+  }
+}
+
 // Weight gradient: partial[(blockIdx.x * C + c) * K + k] = sum over the
 // workgroup's images of dy * x[tap k + output] (Eq. 1 differentiated in w),
 // reduced over lanes and waves in a fixed order (no atomics).
@@ -626,7 +702,6 @@ __global__ __launch_bounds__(kThreads) void strip_wgrad(Params P, const T* __res
   extern __shared__ float smem[];
   Prog* pg = reinterpret_cast<Prog*>(smem);
   float* tiles = smem + kProgWords;
-  float* red = smem + P.trash - kWaves * 64;  // per-wave cell sums, just below the trash area
   const int c = blockIdx.y;
   const int tid = threadIdx.x, lane = tid & 63;
   const int wave = __builtin_amdgcn_readfirstlane(tid >> 6);
@@ -664,24 +739,120 @@ __global__ __launch_bounds__(kThreads) void strip_wgrad(Params P, const T* __res
     wgrad_groups<T, S, KB, kRd, kNd, 1>(P, ch, smem, xc, dc, n_begin, n_end, stg, xpre, acc);
   else
     wgrad_groups<T, S, KB, kRd, kNd, -1>(P, ch, smem, xc, dc, n_begin, n_end, stg, xpre, acc);
-  // lanes -> per-wave cell sums -> per-tap partial of this workgroup, in a fixed order
+  write_partial<KB>(P, pg, smem + P.trash - kWaves * 64, ch.ncells, acc, partial);
+}
+
+// ---------------------------------------------------------------- fused backward
+
+// The group loop of the fused backward.  Per group the tile holds x first
+// (every lane copies the x of its block into registers; the margins give
+// zeros outside the plane), then dy, which the lanes walk with the mirrored
+// program: the walk accumulates the lane's input-gradient block and, per
+// cell, the dot product of the lane's x with the cell's dy values, which is
+// the weight gradient of the cell's taps (Eq. 1 differentiated in w, with
+// the output position moved onto x).  The input gradient leaves through
+// the tile as in gather_groups.  A group's dy is loaded while the lanes
+// copy its x, the next group's x after the walk (no staging registers stay
+// live through the walk, which needs them for the second block).
+template <typename T, int S, int KB, int R, int NC, int SD>
+__device__ __forceinline__ void bwd_groups(const Params& P, const Chan& ch, float* smem, const T* xc, const T* dc,
+                                           T* dxc, int n_begin, int n_end, Stage<T>& stg,
+                                           uint32_t (&pre)[Stage<T>::kWords], float (&acc)[KB]) {
+  constexpr int ST = S + SD;
+  const size_t img = (size_t)P.C * P.H * P.W;
+  float* tiles = smem + kProgWords;
+  const Block bk = block_of<S, R, NC, SD>(P, ch, tiles);
+  for (int n0 = n_begin; n0 < n_end; n0 += P.G) {
+    const int ng = min(P.G, n_end - n0);
+    // dy of the group, in flight while the lanes copy x
+    stg.load(P, dc + (size_t)n0 * img, ng, pre);
+    // the tile holds x of the group
+    float xv[R][NC];
 #pragma unroll
-  for (int ci = 0; ci < KB; ++ci) {
-    if (ci < ch.ncells) {
-      float v = acc[ci];
+    for (int i = 0; i < R; ++i)
 #pragma unroll
-      for (int m = 32; m >= 1; m >>= 1) v += __shfl_xor(v, m, 64);
-      if (lane == 0) red[wave * 64 + ci] = v;
-    }
+      for (int k = 0; k < NC; ++k) xv[i][k] = bk.task ? lds_load(bk.lb + 4 * (i * ST + k)) : 0.f;
+    __syncthreads();  // every lane has its x
+    stg.store_lds(P, S, ch.tr != 0, pre);
+    __syncthreads();  // dy of the group is in the tile
+    // the next group's x (past the end: an empty range, see gather_groups)
+    const int nn = max(0, min(P.G, n_end - n0 - P.G));
+    const size_t next = (size_t)(nn > 0 ? n0 + P.G : n_begin) * img;
+    float out[R][NC];
+#pragma unroll
+    for (int i = 0; i < R; ++i)
+#pragma unroll
+      for (int k = 0; k < NC; ++k) out[i][k] = 0.f;
+    float sl[R + 1][NC];
+    uint32_t base = bk.lb;
+    BwdWalk<R, NC, ST, 0, KB - 1, KB>::run(ch.ncells, base, bk.lb, ch.vrb, ch.bits_lo, ch.bits_hi, ch.vw, sl, xv, out,
+                                          acc);
+    asm volatile("s_waitcnt lgkmcnt(0)" ::: "memory");
+    stg.load(P, xc + next, nn, pre);
+    __syncthreads();  // every lane has finished reading the tile
+    if (bk.task && bk.g < ng) put_block<R, NC, ST, SD>(bk, ch, out);
+    __syncthreads();  // the group's input gradient is in the tile
+    float e[Stage<T>::kQ][4];
+    stg.read_lds(P, S, ch.tr != 0, e);
+    __syncthreads();  // the tile is free
+    stg.store_lds(P, S, ch.tr != 0, pre);  // past the end: zeros into a tile nobody reads
+    stg.store(P, dxc + (size_t)n0 * img, ng, e);
+    __syncthreads();  // x of the next group is in the tile
   }
+}
+
+// Fused backward: dx (the input gradient, stored like the gather's output)
+// and partial[(blockIdx.x * C + c) * K + k] (the workgroup's weight-gradient
+// sum of tap k) from one staging of x and dy per plane and one walk.
+template <typename T, int S, int KB>
+__global__ __launch_bounds__(kThreads) void strip_bwd(Params P, const T* __restrict__ x, const T* __restrict__ dy,
+                                                      const T* __restrict__ wgt, const float* __restrict__ theta,
+                                                      T* __restrict__ dx, float* __restrict__ partial) {
+  extern __shared__ float smem[];
+  Prog* pg = reinterpret_cast<Prog*>(smem);
+  float* tiles = smem + kProgWords;
+  const int c = blockIdx.y;
+  const int tid = threadIdx.x, lane = tid & 63;
+  const int wave = __builtin_amdgcn_readfirstlane(tid >> 6);
+  const size_t HW = (size_t)P.H * P.W;
+  const size_t img = (size_t)P.C * HW;
+  const int n_begin = blockIdx.x * P.npw;
+  const int n_end = min(P.N, n_begin + P.npw);
+  const T* xc = x + (size_t)c * HW;
+  const T* dc = dy + (size_t)c * HW;
+  T* dxc = dx + (size_t)c * HW;
+
+  Stage<T> stg;
+  stg.init_global(P);
+  uint32_t pre[Stage<T>::kWords];
+  stg.load(P, xc + (size_t)n_begin * img, min(P.G, n_end - n_begin), pre);
+  for (int i = tid; i < P.G * P.PS; i += kThreads) tiles[i] = 0.f;  // margins and guards stay zero
+  if (wave == 0) build_prog<T>(pg, wgt, theta[c], c, P.K, -1, P.H, P.W, S);
   __syncthreads();
-  for (int k = tid; k < P.K; k += kThreads) {
-    const int ci = pg->tap_cell[k];
-    float v = 0.f;
-    if (ci >= 0 && ci < KB)
-      for (int w = 0; w < kWaves; ++w) v += red[w * 64 + ci];
-    partial[((size_t)blockIdx.x * P.C + c) * (size_t)P.K + k] = pg->finite ? v : __builtin_nanf("");
-  }
+  Chan ch;
+  ch.tr = __builtin_amdgcn_readfirstlane(pg->tr);
+  ch.s = __builtin_amdgcn_readfirstlane(pg->s);
+  // odd K <= KB: at most KB - 1 cells
+  ch.ncells = min(__builtin_amdgcn_readfirstlane(pg->ncells), KB - 1);
+  ch.bits_lo = __builtin_amdgcn_readfirstlane(pg->brk[0]);
+  ch.bits_hi = __builtin_amdgcn_readfirstlane(pg->brk[1]);
+  ch.vrb = (uint32_t)pg->rbase[lane];
+  ch.vw = __float_as_uint(pg->w[lane]);
+  ch.Hs = ch.tr ? P.W : P.H;
+  ch.Ws = ch.tr ? P.H : P.W;
+  stg.init_lds(P, S, ch.tr != 0, lds_addr(tiles), lds_addr(smem + P.trash));
+  stg.store_lds(P, S, ch.tr != 0, pre);
+  __syncthreads();  // x of the first group is in the tile
+  float acc[KB];
+#pragma unroll
+  for (int i = 0; i < KB; ++i) acc[i] = 0.f;
+  if (ch.s == 0)
+    bwd_groups<T, S, KB, kRv, kNv, 0>(P, ch, smem, xc, dc, dxc, n_begin, n_end, stg, pre, acc);
+  else if (ch.s > 0)
+    bwd_groups<T, S, KB, kRd, kNd, 1>(P, ch, smem, xc, dc, dxc, n_begin, n_end, stg, pre, acc);
+  else
+    bwd_groups<T, S, KB, kRd, kNd, -1>(P, ch, smem, xc, dc, dxc, n_begin, n_end, stg, pre, acc);
+  write_partial<KB>(P, pg, smem + P.trash - kWaves * 64, ch.ncells, acc, partial);
 }
 
 // dw[i] = sum over the partial rows, in a fixed order.
@@ -777,6 +948,33 @@ hipError_t wgrad_t(const Plan& pl, const void* x, const void* dy, const float* t
   hipError_t e = hipErrorInvalidValue;
 #define O1D_CASE(SV) \
   if (pl.S == SV) e = wgrad_launch<T, SV, KB>(pl, x, dy, theta, partial, stream);
+  O1D_STRIP_STRIDES(O1D_CASE)
+#undef O1D_CASE
+  if (e != hipSuccess) return e;
+  const int CK = pl.p.C * pl.p.K;
+  hipLaunchKernelGGL(strip_wgrad_reduce<T>, dim3((unsigned)((CK + 255) / 256)), dim3(256), 0, stream, partial,
+                     static_cast<T*>(dw), CK, pl.blocks_n);
+  return hipGetLastError();
+}
+
+template <typename T, int S, int KB>
+hipError_t bwd_launch(const Plan& pl, const void* x, const void* dy, const void* w, const float* theta, void* dx,
+                      float* partial, hipStream_t stream) {
+  hipError_t e = hipFuncSetAttribute(reinterpret_cast<const void*>(strip_bwd<T, S, KB>),
+                                     hipFuncAttributeMaxDynamicSharedMemorySize, (int)kMaxLdsBytes);
+  if (e != hipSuccess) return e;
+  hipLaunchKernelGGL((strip_bwd<T, S, KB>), dim3((unsigned)pl.blocks_n, (unsigned)pl.p.C, 1), dim3(kThreads),
+                     pl.lds_bytes, stream, pl.p, static_cast<const T*>(x), static_cast<const T*>(dy),
+                     static_cast<const T*>(w), theta, static_cast<T*>(dx), partial);
+  return hipGetLastError();
+}
+
+template <typename T, int KB>
+hipError_t bwd_t(const Plan& pl, const void* x, const void* dy, const void* w, const float* theta, void* dx,
+                 void* dw, float* partial, hipStream_t stream) {
+  hipError_t e = hipErrorInvalidValue;
+#define O1D_CASE(SV) \
+  if (pl.S == SV) e = bwd_launch<T, SV, KB>(pl, x, dy, w, theta, dx, partial, stream);
   O1D_STRIP_STRIDES(O1D_CASE)
 #undef O1D_CASE
   if (e != hipSuccess) return e;

@@ -79,8 +79,28 @@ def bwd_weight(x: torch.Tensor, dy: torch.Tensor, theta: torch.Tensor, K: int, o
     return dw
 
 
+def bwd(x: torch.Tensor, dy: torch.Tensor, w: torch.Tensor, theta: torch.Tensor,
+        out: tuple[torch.Tensor, torch.Tensor] | None = None,
+        workspace: torch.Tensor | None = None) -> tuple[torch.Tensor, torch.Tensor]:
+    """(dx, dw) given x and dy: both adjoints of Eq. 1 in one call."""
+    if dy.shape != x.shape or dy.dtype != x.dtype:
+        raise ValueError("x and dy must have the same shape and dtype")
+    N, C, H, W, K = _check_common(x, w, theta)
+    if not dy.is_cuda or not dy.is_contiguous():
+        raise ValueError("tensors must be contiguous and on the GPU")
+    dx, dw = (torch.empty_like(x), torch.empty_like(w)) if out is None else out
+    need = workspace_bytes(N, C, H, W, K, x.dtype)
+    if workspace is None:
+        workspace = torch.empty(max(need, 1), dtype=torch.uint8, device=x.device)
+    nbytes = workspace.numel() * workspace.element_size()
+    _lib.check("o1d_bwd", _lib.call("o1d_bwd", x.data_ptr(), dy.data_ptr(), w.data_ptr(), theta.data_ptr(),
+                                    dx.data_ptr(), dw.data_ptr(), N, C, H, W, K, _dt(x), workspace.data_ptr(),
+                                    nbytes, _stream(x)))
+    return dx, dw
+
+
 class OrientedConv1dFunction(torch.autograd.Function):
-    """Autograd glue: forward -> o1d_fwd, backward -> o1d_bwd_input + o1d_bwd_weight (theta gets no gradient)."""
+    """Autograd glue: forward -> o1d_fwd, backward -> o1d_bwd (or one of its halves); theta gets no gradient."""
 
     @staticmethod
     def forward(ctx, x, w, theta):
@@ -91,6 +111,9 @@ class OrientedConv1dFunction(torch.autograd.Function):
     def backward(ctx, gy):
         x, w, theta = ctx.saved_tensors
         gy = gy.contiguous()
+        if ctx.needs_input_grad[0] and ctx.needs_input_grad[1]:
+            gx, gw = bwd(x, gy, w, theta)
+            return gx, gw, None
         gx = bwd_input(gy, w, theta) if ctx.needs_input_grad[0] else None
         gw = bwd_weight(x, gy, theta, w.shape[1]) if ctx.needs_input_grad[1] else None
         return gx, gw, None

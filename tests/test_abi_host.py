@@ -30,7 +30,7 @@ def declared_functions():
 
 def test_header_declares_the_abi():
     names = declared_functions()
-    assert {"o1d_fwd", "o1d_bwd_input", "o1d_bwd_weight", "o1d_bwd_weight_workspace_bytes",
+    assert {"o1d_fwd", "o1d_bwd_input", "o1d_bwd_weight", "o1d_bwd", "o1d_bwd_weight_workspace_bytes",
             "o1d_status_str", "o1d_last_error", "o1d_version"} <= set(names)
 
 
@@ -91,6 +91,36 @@ def test_workspace_size_and_rejection():
     assert st == INVALID
     st = _lib.call("o1d_bwd_weight", P, Q, R, None, 2, 3, 5, 6, 7, F32, None, 0, None)
     assert st == INVALID
+
+
+DX, DW, WS, WT = (ctypes.c_void_p(a) for a in (0x200000000, 0x300000000, 0x400000000, 0x500000000))
+
+
+def bwd(*, x=P, dy=Q, w=WT, th=R, dx=DX, dw=DW, N=64, C=96, H=56, W=56, K=31, dt=F32, ws=WS, nbytes=None):
+    if nbytes is None:
+        nbytes = _lib.lib().o1d_bwd_weight_workspace_bytes(N, C, H, W, K, dt)
+    return _lib.call("o1d_bwd", x, dy, w, th, dx, dw, N, C, H, W, K, dt, ws, nbytes, None)
+
+
+@pytest.mark.parametrize("kw,status", [
+    (dict(K=30), INVALID), (dict(N=-1), INVALID), (dict(dt=5), INVALID),
+    (dict(x=None), INVALID), (dict(dy=None), INVALID), (dict(w=None), INVALID), (dict(th=None), INVALID),
+    (dict(dx=None), INVALID), (dict(dw=None), INVALID),
+    (dict(dx=P), INVALID),                                          # dx aliases x
+    (dict(dx=ctypes.c_void_p(0x90000000 + 4096)), INVALID),         # dx overlaps dy
+    (dict(dw=ctypes.c_void_p(0x200000000 + 64)), INVALID),          # dw inside dx
+    (dict(dw=WT), INVALID),                                         # dw aliases w
+    (dict(ws=ctypes.c_void_p(0x200000000)), INVALID),               # workspace aliases dx
+    (dict(ws=None), WORKSPACE), (dict(nbytes=16), WORKSPACE),
+    (dict(K=_lib.MAX_K + 2), UNSUPPORTED), (dict(C=70000), UNSUPPORTED),
+])
+def test_fused_backward_rejects(kw, status):
+    assert bwd(**kw) == status
+    assert _lib.lib().o1d_last_error().decode().startswith("o1d_bwd")
+
+
+def test_fused_backward_without_channels_is_a_noop():
+    assert bwd(C=0, x=None, dy=None, w=None, th=None, dx=None, dw=None, ws=None, nbytes=0) == OK
 
 
 def test_python_wrapper_refuses_cpu_tensors():

@@ -40,7 +40,7 @@ def torch_dtype(name):
     return torch.float32 if name == "f32" else torch.bfloat16
 
 
-def run_case(wl, ops_to_check=("fwd", "bwd_input", "bwd_weight"), inputs=None, label=""):
+def run_case(wl, ops_to_check=("fwd", "bwd_input", "bwd_weight", "bwd"), inputs=None, label=""):
     print(f"[parity] {label or wl.name}: N={wl.N} C={wl.C} H={wl.H} W={wl.W} K={wl.K} {wl.dtype} "
           f"theta={wl.theta} ops={ops_to_check}", flush=True)
     d = synth.make_inputs(wl) if inputs is None else inputs
@@ -53,14 +53,31 @@ def run_case(wl, ops_to_check=("fwd", "bwd_input", "bwd_weight"), inputs=None, l
         y = ops.fwd(x, w, th)
         torch.cuda.synchronize()
         res["fwd"] = err(host(y), oracle.fwd(d["x"], d["w"], d["theta"]))
+    ref = {}
+
+    def ref_dx():
+        if "dx" not in ref:
+            ref["dx"] = oracle.bwd_input(d["dy"], d["w"], d["theta"])
+        return ref["dx"]
+
+    def ref_dw():
+        if "dw" not in ref:
+            ref["dw"] = oracle.bwd_weight(d["x"], d["dy"], d["theta"], wl.K)
+        return ref["dw"]
+
     if "bwd_input" in ops_to_check:
         dx = ops.bwd_input(dy, w, th)
         torch.cuda.synchronize()
-        res["bwd_input"] = err(host(dx), oracle.bwd_input(d["dy"], d["w"], d["theta"]))
+        res["bwd_input"] = err(host(dx), ref_dx())
     if "bwd_weight" in ops_to_check:
         dw = ops.bwd_weight(x, dy, th, wl.K)
         torch.cuda.synchronize()
-        res["bwd_weight"] = err(host(dw), oracle.bwd_weight(d["x"], d["dy"], d["theta"], wl.K))
+        res["bwd_weight"] = err(host(dw), ref_dw())
+    if "bwd" in ops_to_check:  # both gradients from one call
+        fdx, fdw = ops.bwd(x, dy, w, th)
+        torch.cuda.synchronize()
+        res["bwd.dx"] = err(host(fdx), ref_dx())
+        res["bwd.dw"] = err(host(fdw), ref_dw())
     print(f"[parity] {label or wl.name}: " + " ".join(f"{k}={v:.2e}" for k, v in res.items()), flush=True)
     for k, v in res.items():
         assert v <= tol, f"{label or wl.name} {k}: err {v:.3e} > {tol}"
@@ -183,6 +200,15 @@ def test_misaligned_base_pointers():
     torch.cuda.synchronize()
     assert err(host(y), oracle.fwd(d["x"], d["w"], d["theta"])) <= 1e-5
     assert torch.isnan(yb[0])  # the element before the output was not touched
+    # the fused backward with misaligned tensors takes the separate kernels
+    dyb = torch.zeros(n + 1, device=DEV); dyb[1:] = torch.from_numpy(d["dy"].ravel()).to(DEV)
+    dy = dyb[1:].view(d["x"].shape)
+    dxb = torch.full((n + 1,), float("nan"), device=DEV)
+    dx, dw = ops.bwd(x, dy, w, th, out=(dxb[1:].view(d["x"].shape), torch.empty_like(w)))
+    torch.cuda.synchronize()
+    assert err(host(dx), oracle.bwd_input(d["dy"], d["w"], d["theta"])) <= 1e-5
+    assert err(host(dw), oracle.bwd_weight(d["x"], d["dy"], d["theta"], wl.K)) <= 1e-5
+    assert torch.isnan(dxb[0])
 
 
 def test_outputs_fully_written_and_guard_regions_intact():
@@ -204,6 +230,20 @@ def test_outputs_fully_written_and_guard_regions_intact():
     torch.cuda.synchronize()
     assert not torch.isnan(buf[g:g + ck]).any()
     assert torch.isnan(buf[:g]).all() and torch.isnan(buf[g + ck:]).all()
+    # the fused backward, on a shape its one-pass kernel takes (W % 4 == 0)
+    wl = synth.Workload("guard", 3, 7, 36, 40, 31, "f32", "uniform", "fwd+bwd", 15)
+    d = synth.make_inputs(wl)
+    x, dy = dev_tensor(d["x"], torch.float32), dev_tensor(d["dy"], torch.float32)
+    w = dev_tensor(d["w"], torch.float32)
+    th = torch.from_numpy(d["theta"]).to(DEV)
+    n, ck = d["x"].size, wl.C * wl.K
+    bx = torch.full((n + 2 * g,), float("nan"), device=DEV)
+    bw = torch.full((ck + 2 * g,), float("nan"), device=DEV)
+    ops.bwd(x, dy, w, th, out=(bx[g:g + n].view(d["x"].shape), bw[g:g + ck].view(wl.C, wl.K)))
+    torch.cuda.synchronize()
+    for b, m in ((bx, n), (bw, ck)):
+        assert not torch.isnan(b[g:g + m]).any()
+        assert torch.isnan(b[:g]).all() and torch.isnan(b[g + m:]).all()
 
 
 def test_bitwise_reproducible():
@@ -213,8 +253,8 @@ def test_bitwise_reproducible():
     x, dy = dev_tensor(d["x"], torch.float32), dev_tensor(d["dy"], torch.float32)
     w = dev_tensor(d["w"], torch.float32)
     th = torch.from_numpy(d["theta"]).to(DEV)
-    a = [ops.fwd(x, w, th), ops.bwd_input(dy, w, th), ops.bwd_weight(x, dy, th, wl.K)]
-    b = [ops.fwd(x, w, th), ops.bwd_input(dy, w, th), ops.bwd_weight(x, dy, th, wl.K)]
+    a = [ops.fwd(x, w, th), ops.bwd_input(dy, w, th), ops.bwd_weight(x, dy, th, wl.K), *ops.bwd(x, dy, w, th)]
+    b = [ops.fwd(x, w, th), ops.bwd_input(dy, w, th), ops.bwd_weight(x, dy, th, wl.K), *ops.bwd(x, dy, w, th)]
     torch.cuda.synchronize()
     for u, v in zip(a, b):
         assert torch.equal(u, v)
@@ -228,10 +268,12 @@ def test_nonfinite_angle_poisons_only_its_channel():
     w = dev_tensor(d["w"], torch.float32)
     th = torch.from_numpy(d["theta"]).to(DEV)
     y, dx, dw = ops.fwd(x, w, th), ops.bwd_input(dy, w, th), ops.bwd_weight(x, dy, th, wl.K)
+    fdx, fdw = ops.bwd(x, dy, w, th)
     torch.cuda.synchronize()
-    for t in (y, dx):
+    for t in (y, dx, fdx):
         assert torch.isnan(t[:, 2]).all() and not torch.isnan(t[:, [0, 1, 3]]).any()
-    assert torch.isnan(dw[2]).all() and not torch.isnan(dw[[0, 1, 3]]).any()
+    for t in (dw, fdw):
+        assert torch.isnan(t[2]).all() and not torch.isnan(t[[0, 1, 3]]).any()
     keep = [0, 1, 3]
     ref = oracle.fwd(d["x"][:, keep], d["w"][keep], d["theta"][keep])
     assert err(host(y)[:, keep], ref) <= 1e-5
@@ -247,6 +289,10 @@ def test_empty_inputs():
     ops.bwd_weight(x, x, th, 7, out=dw)
     torch.cuda.synchronize()
     assert torch.equal(dw, torch.zeros_like(dw))  # empty sum
+    dw.fill_(float("nan"))
+    ops.bwd(x, x, w, th, out=(torch.empty_like(x), dw))
+    torch.cuda.synchronize()
+    assert torch.equal(dw, torch.zeros_like(dw))
 
 
 def test_autograd_function_matches_oracle():
@@ -261,3 +307,21 @@ def test_autograd_function_matches_oracle():
     assert err(host(y.detach()), oracle.fwd(d["x"], d["w"], d["theta"])) <= 1e-5
     assert err(host(x.grad), oracle.bwd_input(d["dy"], d["w"], d["theta"])) <= 1e-5
     assert err(host(w.grad), oracle.bwd_weight(d["x"], d["dy"], d["theta"], wl.K)) <= 1e-5
+
+
+def test_fused_backward_matches_separate_calls():
+    # the one-pass kernel walks the input gradient's program (same cells,
+    # weights and per-output order as the separate call), so dx agrees
+    # bitwise; dw sums the same products in another order
+    for dtype in ("f32", "bf16"):
+        wl = synth.WORKLOADS["metric"].replace(N=6, dtype=dtype)
+        d = synth.make_inputs(wl)
+        dt = torch_dtype(dtype)
+        x, dy, w = dev_tensor(d["x"], dt), dev_tensor(d["dy"], dt), dev_tensor(d["w"], dt)
+        th = torch.from_numpy(d["theta"]).to(DEV)
+        dx, dw = ops.bwd_input(dy, w, th), ops.bwd_weight(x, dy, th, wl.K)
+        fdx, fdw = ops.bwd(x, dy, w, th)
+        torch.cuda.synchronize()
+        print(f"[fused] {dtype}: dx equal={torch.equal(dx, fdx)} dw err={err(host(fdw), host(dw)):.2e}", flush=True)
+        assert torch.equal(dx, fdx)
+        assert err(host(fdw), host(dw)) <= TOL[dtype]
