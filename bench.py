@@ -1,18 +1,19 @@
 #!/usr/bin/env python3
 """Throughput benchmark of oriented 1D depthwise convolution on one MI355X.
 
-One step = the whole hot path on one batch: forward (o1d_fwd), input gradient
-(o1d_bwd_input) and weight gradient (o1d_bwd_weight), on the headline workload
-64 x 96 x 56 x 56, K = 31, float32, per-channel angles drawn from the eight
-directions i * 22.5 degrees (ConvNeXt-T stage-1 shape, synthetic data).
+One step = the whole hot path on one batch: forward (o1d_fwd), then input and
+weight gradients (o1d_bwd, one pass over x and dy for both), on the headline
+workload 64 x 96 x 56 x 56, K = 31, float32, per-channel angles drawn from the
+eight directions i * 22.5 degrees (ConvNeXt-T stage-1 shape, synthetic data).
 
 Inputs are resident in HBM when the timed region starts.  Steps rotate over
 several disjoint buffer sets whose total size far exceeds the 256 MB
 Infinity Cache, so a step never finds its inputs cached by an earlier step.
 
-Prints ONE JSON line: value = algorithmic bytes of the step (each op reads one
-tensor and writes one, or reads two: 6 tensors of N*C*H*W elements) divided
-by the measured time, in GB/s.  The "roofline" object reports the dominant
+Prints ONE JSON line: value = algorithmic bytes of the step divided by the
+measured time, in GB/s.  The forward reads x and writes y; the backward reads
+x and dy and writes dx (and the C*K weight gradient): 5 tensors of N*C*H*W
+elements.  The "roofline" object reports the dominant
 kernel's algorithmic bytes per launch over its mean duration (HIP events on
 the stream it runs on) against the 8 TB/s HBM peak; "cpu_baseline" times the
 float64 CPU oracle on the same workload.
@@ -55,7 +56,7 @@ def parse():
     ap.add_argument("--no-cpu", action="store_true", help="skip the CPU oracle baseline")
     ap.add_argument("--cpu-seconds", type=float, default=12.0, help="target CPU work for the oracle sample")
     ap.add_argument("--angle-sweep", action="store_true", help="time every K of the angle-cost sweep")
-    ap.add_argument("--only", default="", help="profiling aid: run only this op (fwd|bwd_input|bwd_weight), or "
+    ap.add_argument("--only", default="", help="profiling aid: run only this op (fwd|bwd|bwd_input|bwd_weight), or "
                     "'copy': a plain elementwise copy of one N*C*H*W tensor (reads T bytes, writes T bytes), "
                     "the calibration kernel for the HBM byte counters")
     return ap.parse_args()
@@ -83,9 +84,11 @@ def run_ops(ops, b, K, only=""):
         return
     if not only or only == "fwd":
         ops.fwd(b.x, b.w, b.th, out=b.y)
-    if not only or only == "bwd_input":
+    if not only or only == "bwd":
+        ops.bwd(b.x, b.dy, b.w, b.th, out=(b.dx, b.dw), workspace=b.ws)
+    if only == "bwd_input":
         ops.bwd_input(b.dy, b.w, b.th, out=b.dx)
-    if not only or only == "bwd_weight":
+    if only == "bwd_weight":
         ops.bwd_weight(b.x, b.dy, b.th, K, out=b.dw, workspace=b.ws)
 
 
@@ -96,7 +99,7 @@ def time_workload(wl, steps, warmup, nsets, torch, ops, synth, only="", per_op=T
     sets = [BufferSet(d, wl, torch, dev, ops) for _ in range(nsets)]
     for i in range(warmup):
         run_ops(ops, sets[i % nsets], wl.K, only)
-    names = [only] if only else ["fwd", "bwd_input", "bwd_weight"]
+    names = [only] if only else ["fwd", "bwd"]
     stream = torch.cuda.current_stream(dev)
     ev = []
     torch.cuda.synchronize()
@@ -140,13 +143,13 @@ def cpu_baseline(wl, synth, seconds):
         oracle.bwd_weight(x, dy, th, wl.K, threads)
         t_total += time.perf_counter() - t0
         reps += 1
-    step_bytes = 6 * wl.elems * wl.elem_bytes
+    step_bytes = 5 * wl.elems * wl.elem_bytes + wl.C * wl.K * wl.elem_bytes  # as the GPU step
     return {
         "value": round(step_bytes * reps / t_total / 1e9, 3),
         "unit": "GB/s",
         "cores": threads,
         "kind": "oracle",
-        "sample": f"{reps} full step(s) of the same workload (fwd + bwd_input + bwd_weight, "
+        "sample": f"{reps} full step(s) of the same workload (fwd, then dx and dw, "
                   f"{wl.N}x{wl.C}x{wl.H}x{wl.W}, K={wl.K}) in float64 C loops, OpenMP over planes/channels; "
                   f"{t_total:.1f} s",
         "ms_per_step": round(t_total * 1e3 / reps, 1),
@@ -185,7 +188,8 @@ def main():
     ms, durs = time_workload(wl, args.steps, args.warmup, args.sets, torch, ops, synth, args.only)
     print(f"[bench] {ms:.4f} ms/step", file=sys.stderr, flush=True)
 
-    op_bytes = {"fwd": 2 * T, "bwd_input": 2 * T, "bwd_weight": 2 * T + wl.C * wl.K * wl.elem_bytes, "copy": 2 * T}
+    CK = wl.C * wl.K * wl.elem_bytes
+    op_bytes = {"fwd": 2 * T, "bwd": 3 * T + CK, "bwd_input": 2 * T, "bwd_weight": 2 * T + CK, "copy": 2 * T}
     per_op = {}
     for nm, v in durs.items():
         mean = statistics.fmean(v)
@@ -215,7 +219,7 @@ def main():
         "data": "synthetic",
         "config": {
             "workload": f"{wl.name}: N={wl.N} C={wl.C} H={wl.H} W={wl.W} K={wl.K} {wl.dtype}, theta from the 8 "
-                        f"directions i*22.5 deg, one step = fwd + bwd_input + bwd_weight",
+                        f"directions i*22.5 deg, one step = fwd + bwd (dx and dw in one pass)",
             "N": wl.N, "C": wl.C, "H": wl.H, "W": wl.W, "K": wl.K,
             "buffer_sets": args.sets,
             "step_bytes": step_bytes,
