@@ -101,26 +101,35 @@ def time_workload(wl, steps, warmup, nsets, torch, ops, synth, only="", per_op=T
         run_ops(ops, sets[i % nsets], wl.K, only)
     names = [only] if only else ["fwd", "bwd"]
     stream = torch.cuda.current_stream(dev)
+    # One event before every op; the event before a step's first op also ends
+    # the previous step's last op, and one more event ends the last step.
     ev = []
+
+    def mark():
+        e = torch.cuda.Event(enable_timing=True)
+        e.record(stream)
+        ev.append(e)
+
     torch.cuda.synchronize()
     t0 = time.perf_counter()
     for i in range(steps):
         b = sets[i % nsets]
         if per_op:
-            marks = [torch.cuda.Event(enable_timing=True) for _ in range(len(names) + 1)]
-            marks[0].record(stream)
-            for j, nm in enumerate(names):
+            for nm in names:
+                mark()
                 run_ops(ops, b, wl.K, nm)
-                marks[j + 1].record(stream)
-            ev.append(marks)
         else:
             run_ops(ops, b, wl.K, only)
+    if per_op:
+        mark()
     torch.cuda.synchronize()
     t1 = time.perf_counter()
     durs = {nm: [] for nm in names}
-    for marks in ev:
-        for j, nm in enumerate(names):
-            durs[nm].append(marks[j].elapsed_time(marks[j + 1]))
+    if per_op:
+        for i in range(steps):
+            for j, nm in enumerate(names):
+                k = i * len(names) + j
+                durs[nm].append(ev[k].elapsed_time(ev[k + 1]))
     del sets
     torch.cuda.empty_cache()
     return (t1 - t0) * 1e3 / steps, durs
