@@ -35,6 +35,13 @@ METRIC = "oriented-1D DW conv fwd+bwd ms & GB/s (% HBM peak), K=31, 64×96×56×
 HBM_PEAK_GBS = 8000.0
 CSRC = os.path.join(ROOT, "paper_2309_15812_amd", "csrc")
 TRAFFIC_FILE = os.path.join(ROOT, "profiles", "traffic_metric_workload.json")
+THETA_TEXT = {
+    "discrete8": "theta from the 8 directions i*22.5 deg",
+    "uniform": "theta uniform in [0, 180) deg per channel",
+    "zero": "theta = 0 for every channel",
+    "ninety": "theta = 90 deg for every channel",
+    "ramp": "theta_c = 22.5 c deg",
+}
 
 
 def kernel_source_hash() -> str:
@@ -227,8 +234,9 @@ def main():
         "dtype": wl.dtype,
         "data": "synthetic",
         "config": {
-            "workload": f"{wl.name}: N={wl.N} C={wl.C} H={wl.H} W={wl.W} K={wl.K} {wl.dtype}, theta from the 8 "
-                        f"directions i*22.5 deg, one step = fwd + bwd (dx and dw in one pass)",
+            "workload": f"{wl.name}: N={wl.N} C={wl.C} H={wl.H} W={wl.W} K={wl.K} {wl.dtype}, "
+                        f"{THETA_TEXT.get(wl.theta, 'theta mode ' + wl.theta)}, "
+                        f"one step = fwd + bwd (dx and dw in one pass)",
             "N": wl.N, "C": wl.C, "H": wl.H, "W": wl.W, "K": wl.K,
             "buffer_sets": args.sets,
             "step_bytes": step_bytes,

@@ -73,10 +73,13 @@ inline int fit_npw(int N, int C, int G, long long slots) {
 // start up to R - 1 columns outside the plane); ncg groups of NC adjacent
 // strips per band.  A task = one group of one band of one plane.
 // Lanes per plane (ppt): vertical tasks one per lane, band after band;
-// diagonal tasks in half-wave blocks of 8 column groups x 4 bands.
+// diagonal tasks in half-wave blocks of 8 column groups x 4 bands, unless
+// the plane is so small that the blocks leave enough lanes idle to cost a
+// plane per group: then one per lane, band after band (dense).
 struct Shape {
   int R, NC, nb, nj, jlo, ncg, ppt;
   int bq, bb;  // diagonal: half-wave blocks along the column groups and along the bands
+  int dense;   // tasks one per lane, band after band
 };
 
 __host__ __device__ inline Shape shape_of(int Hs, int Ws, int s) {
@@ -89,7 +92,9 @@ __host__ __device__ inline Shape shape_of(int Hs, int Ws, int s) {
   t.ncg = cdiv(t.nj, t.NC);
   t.bq = cdiv(t.ncg, 8);
   t.bb = cdiv(t.nb, 4);
-  t.ppt = s ? 32 * t.bq * t.bb : t.nb * t.ncg;
+  const int blocked = 32 * t.bq * t.bb, dense = t.nb * t.ncg;
+  t.dense = !s || kThreads / dense > kThreads / blocked;
+  t.ppt = t.dense ? dense : blocked;
   return t;
 }
 

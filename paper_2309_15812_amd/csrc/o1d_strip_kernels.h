@@ -497,7 +497,7 @@ __device__ __forceinline__ Block block_of(const Params& P, const Chan& ch, const
   int g = t / sh.ppt;
   const int r = t - g * sh.ppt;
   int band, cg;
-  if (SD == 0) {
+  if (SD == 0 || sh.dense) {
     band = r / sh.ncg;
     cg = r - band * sh.ncg;
   } else {
