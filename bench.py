@@ -172,6 +172,15 @@ def cpu_baseline(wl, synth, seconds):
     }
 
 
+def algorithmic_bytes(wl) -> dict:
+    """Bytes each op must move (T = one N*C*H*W tensor): the forward reads x
+    and writes y; the fused backward reads x and dy and writes dx and dw; the
+    separate gradients read one or two tensors and write one (or dw)."""
+    T = wl.elems * wl.elem_bytes
+    CK = wl.C * wl.K * wl.elem_bytes
+    return {"fwd": 2 * T, "bwd": 3 * T + CK, "bwd_input": 2 * T, "bwd_weight": 2 * T + CK, "copy": 2 * T}
+
+
 def traffic_for(op_name: str):
     """HBM bytes per launch from the committed rocprofv3 counter summary, if it
     was taken on the current kernel sources."""
@@ -204,8 +213,7 @@ def main():
     ms, durs = time_workload(wl, args.steps, args.warmup, args.sets, torch, ops, synth, args.only)
     print(f"[bench] {ms:.4f} ms/step", file=sys.stderr, flush=True)
 
-    CK = wl.C * wl.K * wl.elem_bytes
-    op_bytes = {"fwd": 2 * T, "bwd": 3 * T + CK, "bwd_input": 2 * T, "bwd_weight": 2 * T + CK, "copy": 2 * T}
+    op_bytes = algorithmic_bytes(wl)
     per_op = {}
     for nm, v in durs.items():
         mean = statistics.fmean(v)
