@@ -325,3 +325,28 @@ def test_fused_backward_matches_separate_calls():
         print(f"[fused] {dtype}: dx equal={torch.equal(dx, fdx)} dw err={err(host(fdw), host(dw)):.2e}", flush=True)
         assert torch.equal(dx, fdx)
         assert err(host(fdw), host(dw)) <= TOL[dtype]
+
+
+def _random_cases(n, seed):
+    rng = np.random.default_rng(seed)
+    cases = []
+    for _ in range(n):
+        H = int(rng.integers(1, 61))
+        W = int(rng.choice([4, 8, 12, 16, 20, 28, 32, 40, 44, 52, 56, 60])) if rng.random() < 0.7 else \
+            int(rng.integers(1, 61))
+        K = int(rng.choice([1, 3, 5, 7, 9, 15, 21, 31, 33, 63]))
+        N, C = int(rng.integers(1, 10)), int(rng.integers(1, 7))
+        mode = str(rng.choice(["uniform", "discrete8", "ramp"]))
+        dtype = "f32" if rng.random() < 0.6 else "bf16"
+        cases.append((N, C, H, W, K, mode, dtype))
+    return cases
+
+
+# Seeded random shapes: small and ragged planes, both staging frames, dense
+# and blocked lane layouts, partial plane groups, walks of up to 63 cells,
+# and the fused backward on and off its one-pass kernel.
+@pytest.mark.parametrize("case", _random_cases(24, 20261202), ids=lambda c: "x".join(map(str, c[:5])) + "-" + c[5] + "-" + c[6])
+def test_random_shapes(case):
+    N, C, H, W, K, mode, dtype = case
+    wl = synth.Workload("random", N, C, H, W, K, dtype, mode, "fwd+bwd", 21)
+    run_case(wl, label=f"random {case}")
