@@ -75,11 +75,16 @@ inline int fit_npw(int N, int C, int G, long long slots) {
 // Lanes per plane (ppt): vertical tasks one per lane, band after band;
 // diagonal tasks in half-wave blocks of 8 column groups x 4 bands, unless
 // the plane is so small that the blocks leave enough lanes idle to cost a
-// plane per group: then one per lane, band after band (dense).
+// plane per group: then one per lane, band after band (dense).  In the
+// band-after-band layouts a band takes lpb >= ncg lanes: rounded up to a
+// whole wave (else half-wave) where that costs no plane per group, so that
+// the lanes of one wave read one band's consecutive columns (two bands in a
+// wave map their columns onto overlapping LDS banks).
 struct Shape {
   int R, NC, nb, nj, jlo, ncg, ppt;
   int bq, bb;  // diagonal: half-wave blocks along the column groups and along the bands
   int dense;   // tasks one per lane, band after band
+  int lpb;     // band-after-band layouts: lanes per band
 };
 
 __host__ __device__ inline Shape shape_of(int Hs, int Ws, int s) {
@@ -94,7 +99,18 @@ __host__ __device__ inline Shape shape_of(int Hs, int Ws, int s) {
   t.bb = cdiv(t.nb, 4);
   const int blocked = 32 * t.bq * t.bb, dense = t.nb * t.ncg;
   t.dense = !s || kThreads / dense > kThreads / blocked;
-  t.ppt = t.dense ? dense : blocked;
+  t.lpb = t.ncg;
+  if (t.dense) {
+    const int planes = kThreads / dense;
+    for (int a = 64; a >= 32; a /= 2) {
+      const int l = cdiv(t.ncg, a) * a;
+      if (t.nb * l <= kThreads && kThreads / (t.nb * l) == planes) {
+        t.lpb = l;
+        break;
+      }
+    }
+  }
+  t.ppt = t.dense ? t.nb * t.lpb : blocked;
   return t;
 }
 

@@ -498,8 +498,8 @@ __device__ __forceinline__ Block block_of(const Params& P, const Chan& ch, const
   const int r = t - g * sh.ppt;
   int band, cg;
   if (SD == 0 || sh.dense) {
-    band = r / sh.ncg;
-    cg = r - band * sh.ncg;
+    band = r / sh.lpb;
+    cg = r - band * sh.lpb;
   } else {
     const int blk = r >> 5, bqi = blk % sh.bq, bbi = blk / sh.bq;
     cg = 8 * bqi + (r & 7);
