@@ -39,10 +39,21 @@ def _check_common(x: torch.Tensor, w: torch.Tensor, theta: torch.Tensor):
     return N, C, H, W, int(w.shape[1])
 
 
+def _out(out: torch.Tensor | None, like: torch.Tensor, shape=None) -> torch.Tensor:
+    """A caller-given output must match what the kernels write (they take no strides or sizes of it)."""
+    shape = tuple(like.shape) if shape is None else tuple(shape)
+    if out is None:
+        return torch.empty(shape, dtype=like.dtype, device=like.device)
+    if tuple(out.shape) != shape or out.dtype != like.dtype or out.device != like.device or not out.is_contiguous():
+        raise ValueError(f"output {tuple(out.shape)} {out.dtype} {out.device} must be a contiguous {shape} "
+                         f"{like.dtype} tensor on {like.device}")
+    return out
+
+
 def fwd(x: torch.Tensor, w: torch.Tensor, theta: torch.Tensor, out: torch.Tensor | None = None) -> torch.Tensor:
     """y = oriented depthwise 1D convolution of x (Definition 1, Eq. 1-2)."""
     N, C, H, W, K = _check_common(x, w, theta)
-    y = torch.empty_like(x) if out is None else out
+    y = _out(out, x)
     _lib.check("o1d_fwd", _lib.call("o1d_fwd", x.data_ptr(), w.data_ptr(), theta.data_ptr(), y.data_ptr(),
                                     N, C, H, W, K, _dt(x), _stream(x)))
     return y
@@ -51,7 +62,7 @@ def fwd(x: torch.Tensor, w: torch.Tensor, theta: torch.Tensor, out: torch.Tensor
 def bwd_input(dy: torch.Tensor, w: torch.Tensor, theta: torch.Tensor, out: torch.Tensor | None = None) -> torch.Tensor:
     """dx given dy (adjoint of Eq. 1 in x)."""
     N, C, H, W, K = _check_common(dy, w, theta)
-    dx = torch.empty_like(dy) if out is None else out
+    dx = _out(out, dy)
     _lib.check("o1d_bwd_input", _lib.call("o1d_bwd_input", dy.data_ptr(), w.data_ptr(), theta.data_ptr(),
                                           dx.data_ptr(), N, C, H, W, K, _dt(dy), _stream(dy)))
     return dx
@@ -67,8 +78,10 @@ def bwd_weight(x: torch.Tensor, dy: torch.Tensor, theta: torch.Tensor, K: int, o
     if dy.shape != x.shape or dy.dtype != x.dtype:
         raise ValueError("x and dy must have the same shape and dtype")
     N, C, H, W = x.shape
-    dw = torch.empty((C, K), dtype=x.dtype, device=x.device) if out is None else out
+    dw = _out(out, x, (C, K))
     _check_common(x, dw, theta)
+    if not dy.is_cuda or not dy.is_contiguous():
+        raise ValueError("tensors must be contiguous and on the GPU")
     need = workspace_bytes(N, C, H, W, K, x.dtype)
     if workspace is None:
         workspace = torch.empty(max(need, 1), dtype=torch.uint8, device=x.device)
@@ -88,7 +101,7 @@ def bwd(x: torch.Tensor, dy: torch.Tensor, w: torch.Tensor, theta: torch.Tensor,
     N, C, H, W, K = _check_common(x, w, theta)
     if not dy.is_cuda or not dy.is_contiguous():
         raise ValueError("tensors must be contiguous and on the GPU")
-    dx, dw = (torch.empty_like(x), torch.empty_like(w)) if out is None else out
+    dx, dw = (_out(None, x), _out(None, w)) if out is None else (_out(out[0], x), _out(out[1], w))
     need = workspace_bytes(N, C, H, W, K, x.dtype)
     if workspace is None:
         workspace = torch.empty(max(need, 1), dtype=torch.uint8, device=x.device)

@@ -350,3 +350,22 @@ def test_random_shapes(case):
     N, C, H, W, K, mode, dtype = case
     wl = synth.Workload("random", N, C, H, W, K, dtype, mode, "fwd+bwd", 21)
     run_case(wl, label=f"random {case}")
+
+
+def test_wrapper_rejects_mismatched_outputs():
+    # the kernels take no strides or sizes of their outputs: the wrapper checks them first
+    x = torch.randn(2, 3, 8, 8, device=DEV)
+    w = torch.randn(3, 5, device=DEV)
+    th = torch.zeros(3, device=DEV)
+    for bad in (torch.empty(2, 3, 8, 7, device=DEV), torch.empty(2, 3, 8, 8, device=DEV, dtype=torch.bfloat16),
+                torch.empty(2, 3, 8, 16, device=DEV)[..., ::2]):
+        with pytest.raises(ValueError):
+            ops.fwd(x, w, th, out=bad)
+        with pytest.raises(ValueError):
+            ops.bwd_input(x, w, th, out=bad)
+        with pytest.raises(ValueError):
+            ops.bwd(x, x, w, th, out=(bad, torch.empty_like(w)))
+    with pytest.raises(ValueError):
+        ops.bwd_weight(x, x, th, 5, out=torch.empty(3, 4, device=DEV))
+    with pytest.raises(ValueError):
+        ops.bwd(x, x, w, th, out=(torch.empty_like(x), torch.empty(3, 4, device=DEV)))
