@@ -506,10 +506,14 @@ __device__ __forceinline__ Block block_of(const Params& P, const Chan& ch, const
     band = 4 * bbi + ((r >> 3) & 3);
   }
   Block bk;
-  bk.task = g < P.G && band < sh.nb && cg < sh.ncg;
-  bk.g = bk.task ? g : 0;
-  bk.b0 = bk.task ? band * R : 0;
-  bk.j0 = bk.task ? sh.jlo + cg * NC : sh.jlo;
+  // a lane past its band's last column group reads that group's addresses
+  // (a broadcast, no extra bank traffic); lanes past the bands or planes
+  // take the first block
+  const bool in_band = g < P.G && band < sh.nb;
+  bk.task = in_band && cg < sh.ncg;
+  bk.g = in_band ? g : 0;
+  bk.b0 = in_band ? band * R : 0;
+  bk.j0 = in_band ? sh.jlo + min(cg, sh.ncg - 1) * NC : sh.jlo;
   bk.lb = lds_addr(tiles + bk.g * P.PS + kGuard + (P.halo + bk.b0) * S + P.mc + bk.j0);
   const int cmin = bk.j0 + (SD < 0 ? -(R - 1) : 0), cmax = bk.j0 + NC - 1 + (SD > 0 ? R - 1 : 0);
   bk.full = bk.b0 + R <= ch.Hs && cmin >= 0 && cmax < ch.Ws;
