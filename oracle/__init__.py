@@ -52,6 +52,12 @@ def _load():
             f = getattr(lib, name)
             f.argtypes = [_D, _D, _D, _D] + [ctypes.c_int] * 6
             f.restype = None
+        for name in ("oracle_fwd_ex", "oracle_bwd_input_ex", "oracle_bwd_weight_ex"):
+            f = getattr(lib, name)
+            f.argtypes = [_D, _D, _D, _D] + [ctypes.c_int] * 8
+            f.restype = None
+        lib.oracle_tap_samples.argtypes = [ctypes.c_double, ctypes.c_int, ctypes.c_int, _I, _I, _D]
+        lib.oracle_tap_samples.restype = None
         _lib = lib
     return _lib
 
@@ -95,33 +101,81 @@ def _check(x, K, C):
         raise ValueError("K must be odd and positive")
 
 
-def fwd(x, w, theta_deg, threads: int | None = None) -> np.ndarray:
-    """y = oriented depthwise 1D convolution of x (N,C,H,W) with w (C,K)."""
+MODES = {"floor": 0, "bilinear": 1}
+
+
+def out_size(n: int, stride: int) -> int:
+    """Output length along one axis for a centred odd kernel: floor((n - 1) / stride) + 1."""
+    return (n - 1) // stride + 1
+
+
+def _plain(stride: int, mode: str) -> bool:
+    if stride < 1:
+        raise ValueError("stride must be >= 1")
+    if mode not in MODES:
+        raise ValueError(f"unknown mode {mode!r}")
+    return stride == 1 and mode == "floor"
+
+
+def tap_samples(theta_deg: float, K: int, mode: str = "floor"):
+    """Per tap, four (row offset, column offset, coefficient) samples: rounding down uses one with
+    coefficient 1, bilinear interpolation the four surrounding pixels."""
+    sh = np.zeros(4 * K, np.int32)
+    sw = np.zeros(4 * K, np.int32)
+    sc = np.zeros(4 * K, np.float64)
+    _load().oracle_tap_samples(float(theta_deg), K, MODES[mode], _ptr(sh, _I), _ptr(sw, _I), _ptr(sc))
+    return sh.reshape(K, 4), sw.reshape(K, 4), sc.reshape(K, 4)
+
+
+def fwd(x, w, theta_deg, threads: int | None = None, stride: int = 1, mode: str = "floor") -> np.ndarray:
+    """y = oriented depthwise 1D convolution of x (N,C,H,W) with w (C,K); y is (N,C,P,Q)."""
     x = _f64(x); w = _f64(w); th = _f64(theta_deg)
     N, C, H, W = x.shape
     K = w.shape[1]
     _check(x, K, C)
-    y = np.empty_like(x)
-    _load().oracle_fwd(_ptr(x), _ptr(w), _ptr(th), _ptr(y), N, C, H, W, K, threads or default_threads())
+    lib, t = _load(), threads or default_threads()
+    if _plain(stride, mode):
+        y = np.empty_like(x)
+        lib.oracle_fwd(_ptr(x), _ptr(w), _ptr(th), _ptr(y), N, C, H, W, K, t)
+        return y
+    y = np.empty((N, C, out_size(H, stride), out_size(W, stride)), np.float64)
+    lib.oracle_fwd_ex(_ptr(x), _ptr(w), _ptr(th), _ptr(y), N, C, H, W, K, stride, MODES[mode], t)
     return y
 
 
-def bwd_input(dy, w, theta_deg, threads: int | None = None) -> np.ndarray:
-    """dL/dx given dL/dy (scatter form of the adjoint of Eq. 1)."""
+def bwd_input(dy, w, theta_deg, threads: int | None = None, stride: int = 1, mode: str = "floor",
+              in_hw: tuple[int, int] | None = None) -> np.ndarray:
+    """dL/dx (N,C,H,W) given dL/dy (N,C,P,Q) (scatter form of the adjoint of Eq. 1).  With stride > 1 the
+    input size (H, W) is not implied by (P, Q) and must be given as in_hw."""
     dy = _f64(dy); w = _f64(w); th = _f64(theta_deg)
-    N, C, H, W = dy.shape
+    N, C, P, Q = dy.shape
     K = w.shape[1]
     _check(dy, K, C)
-    dx = np.empty_like(dy)
-    _load().oracle_bwd_input(_ptr(dy), _ptr(w), _ptr(th), _ptr(dx), N, C, H, W, K, threads or default_threads())
+    lib, t = _load(), threads or default_threads()
+    if _plain(stride, mode) and in_hw in (None, (P, Q)):
+        dx = np.empty_like(dy)
+        lib.oracle_bwd_input(_ptr(dy), _ptr(w), _ptr(th), _ptr(dx), N, C, P, Q, K, t)
+        return dx
+    H, W = (P, Q) if in_hw is None else in_hw
+    if (out_size(H, stride), out_size(W, stride)) != (P, Q):
+        raise ValueError(f"dy {P}x{Q} is not the stride-{stride} output of a {H}x{W} input")
+    dx = np.empty((N, C, H, W), np.float64)
+    lib.oracle_bwd_input_ex(_ptr(dy), _ptr(w), _ptr(th), _ptr(dx), N, C, H, W, K, stride, MODES[mode], t)
     return dx
 
 
-def bwd_weight(x, dy, theta_deg, K: int, threads: int | None = None) -> np.ndarray:
-    """dL/dw (C,K) given the input x and dL/dy (scatter form of the adjoint of Eq. 1)."""
+def bwd_weight(x, dy, theta_deg, K: int, threads: int | None = None, stride: int = 1,
+               mode: str = "floor") -> np.ndarray:
+    """dL/dw (C,K) given the input x (N,C,H,W) and dL/dy (N,C,P,Q) (scatter form of the adjoint of Eq. 1)."""
     x = _f64(x); dy = _f64(dy); th = _f64(theta_deg)
     N, C, H, W = x.shape
     _check(x, K, C)
+    if dy.shape != (N, C, out_size(H, stride), out_size(W, stride)):
+        raise ValueError(f"dy {dy.shape} does not match x {x.shape} at stride {stride}")
+    lib, t = _load(), threads or default_threads()
     dw = np.empty((C, K), np.float64)
-    _load().oracle_bwd_weight(_ptr(x), _ptr(dy), _ptr(th), _ptr(dw), N, C, H, W, K, threads or default_threads())
+    if _plain(stride, mode):
+        lib.oracle_bwd_weight(_ptr(x), _ptr(dy), _ptr(th), _ptr(dw), N, C, H, W, K, t)
+    else:
+        lib.oracle_bwd_weight_ex(_ptr(x), _ptr(dy), _ptr(th), _ptr(dw), N, C, H, W, K, stride, MODES[mode], t)
     return dw

@@ -163,3 +163,172 @@ void oracle_bwd_weight(const double* x, const double* dy, const double* theta_de
     free(dw);
   }
 }
+
+/* ------------------------------------------------------------------------
+ * Extensions: stride and the bilinear-interpolation variant.
+ *
+ * Stride (Definition 1, Eq. 2): the output position (p, q) samples the input
+ * at (str*p + dh_k, str*q + dw_k).  The paper does not give P and Q; the
+ * reading taken here is the usual one for a centred odd kernel,
+ * P = floor((H - 1) / str) + 1 and Q = floor((W - 1) / str) + 1, so that
+ * output (p, q) is centred on input (str*p, str*q).
+ *
+ * Bilinear variant (section "Discretization and Interpolation", where the
+ * paper weighs it against rounding down): tap k samples the input at the
+ * unrounded position (str*p + rh_k, str*q + rw_k), (rh_k, rw_k) =
+ * (-(k - pad) sin theta, (k - pad) cos theta), by bilinear interpolation of
+ * the four surrounding pixels, each read as zero outside the plane:
+ *   h0 = floor(rh), fh = rh - h0, w0 = floor(rw), fw = rw - w0,
+ *   sample = (1-fh)(1-fw) x[h0][w0] + (1-fh) fw x[h0][w0+1]
+ *          + fh (1-fw) x[h0+1][w0] + fh fw x[h0+1][w0+1].
+ * The floor takes reading R2 (a product within 1e-9 of an integer is that
+ * integer, with a zero fraction), which only matters at the 1e-16 level
+ * here since the result is continuous in the fraction.
+ *
+ * Both are written as a list of (row offset, column offset, coefficient)
+ * samples per tap: one sample with coefficient 1 for rounding down, four
+ * for bilinear.  y sums w[c,k] * coefficient * x over every sample; the
+ * backward passes are again the literal adjoints in scatter form.
+ * ------------------------------------------------------------------------ */
+
+/* Samples of the K taps: sh, sw, sc hold 4 entries per tap (unused entries
+ * have coefficient 0).  mode 0 = round down (Eq. 2), 1 = bilinear. */
+static void tap_samples(double theta_deg, int K, int mode, int* sh, int* sw, double* sc) {
+  const int pad = K / 2;
+  double* rh = (double*)malloc(sizeof(double) * (size_t)K);
+  double* rw = (double*)malloc(sizeof(double) * (size_t)K);
+  oracle_offsets_real(theta_deg, K, pad, rh, rw);
+  for (int k = 0; k < K; ++k) {
+    const double h0 = floor_snapped(rh[k]), w0 = floor_snapped(rw[k]);
+    for (int s = 0; s < 4; ++s) {
+      sh[4 * k + s] = (int)h0 + (s >> 1);
+      sw[4 * k + s] = (int)w0 + (s & 1);
+      sc[4 * k + s] = 0.0;
+    }
+    if (mode == 0) {
+      sc[4 * k] = 1.0;
+    } else {
+      /* a snapped coordinate is exactly the integer h0: zero fraction */
+      const double fh = (fabs(rh[k] - h0) <= ORACLE_SNAP_EPS) ? 0.0 : rh[k] - h0;
+      const double fw = (fabs(rw[k] - w0) <= ORACLE_SNAP_EPS) ? 0.0 : rw[k] - w0;
+      sc[4 * k + 0] = (1.0 - fh) * (1.0 - fw);
+      sc[4 * k + 1] = (1.0 - fh) * fw;
+      sc[4 * k + 2] = fh * (1.0 - fw);
+      sc[4 * k + 3] = fh * fw;
+    }
+  }
+  free(rh);
+  free(rw);
+}
+
+/* Exposed for the tests: the sample list of one channel. */
+void oracle_tap_samples(double theta_deg, int K, int mode, int* sh, int* sw, double* sc) {
+  tap_samples(theta_deg, K, mode, sh, sw, sc);
+}
+
+int oracle_out_size(int n, int str) { return (n - 1) / str + 1; }
+
+/* Forward pass with stride and discretisation mode; y is N x C x P x Q. */
+void oracle_fwd_ex(const double* x, const double* wt, const double* theta_deg, double* y,
+                   int N, int C, int H, int W, int K, int str, int mode, int nthreads) {
+  const int P = oracle_out_size(H, str), Q = oracle_out_size(W, str);
+  const long planes = (long)N * C;
+#pragma omp parallel for schedule(dynamic) num_threads(nthreads)
+  for (long nc = 0; nc < planes; ++nc) {
+    const int c = (int)(nc % C);
+    int* sh = (int*)malloc(sizeof(int) * 4 * (size_t)K);
+    int* sw = (int*)malloc(sizeof(int) * 4 * (size_t)K);
+    double* sc = (double*)malloc(sizeof(double) * 4 * (size_t)K);
+    tap_samples(theta_deg[c], K, mode, sh, sw, sc);
+    const double* xp = x + (size_t)nc * H * W;
+    double* yp = y + (size_t)nc * P * Q;
+    for (int p = 0; p < P; ++p) {
+      for (int q = 0; q < Q; ++q) {
+        double acc = 0.0;
+        for (int k = 0; k < K; ++k) {
+          for (int s = 0; s < 4; ++s) {
+            if (sc[4 * k + s] == 0.0) continue;
+            const int h = str * p + sh[4 * k + s];
+            const int w = str * q + sw[4 * k + s];
+            if (h >= 0 && h < H && w >= 0 && w < W)
+              acc += xp[(size_t)h * W + w] * sc[4 * k + s] * wt[(size_t)c * K + k];
+          }
+        }
+        yp[(size_t)p * Q + q] = acc;
+      }
+    }
+    free(sh);
+    free(sw);
+    free(sc);
+  }
+}
+
+/* Gradient with respect to the input (N x C x H x W) given dy (N x C x P x Q). */
+void oracle_bwd_input_ex(const double* dy, const double* wt, const double* theta_deg, double* dx,
+                         int N, int C, int H, int W, int K, int str, int mode, int nthreads) {
+  const int P = oracle_out_size(H, str), Q = oracle_out_size(W, str);
+  const long planes = (long)N * C;
+#pragma omp parallel for schedule(dynamic) num_threads(nthreads)
+  for (long nc = 0; nc < planes; ++nc) {
+    const int c = (int)(nc % C);
+    int* sh = (int*)malloc(sizeof(int) * 4 * (size_t)K);
+    int* sw = (int*)malloc(sizeof(int) * 4 * (size_t)K);
+    double* sc = (double*)malloc(sizeof(double) * 4 * (size_t)K);
+    tap_samples(theta_deg[c], K, mode, sh, sw, sc);
+    const double* gp = dy + (size_t)nc * P * Q;
+    double* xp = dx + (size_t)nc * H * W;
+    memset(xp, 0, sizeof(double) * (size_t)H * W);
+    for (int p = 0; p < P; ++p) {
+      for (int q = 0; q < Q; ++q) {
+        const double g = gp[(size_t)p * Q + q];
+        for (int k = 0; k < K; ++k) {
+          for (int s = 0; s < 4; ++s) {
+            if (sc[4 * k + s] == 0.0) continue;
+            const int h = str * p + sh[4 * k + s];
+            const int w = str * q + sw[4 * k + s];
+            if (h >= 0 && h < H && w >= 0 && w < W)
+              xp[(size_t)h * W + w] += g * sc[4 * k + s] * wt[(size_t)c * K + k];
+          }
+        }
+      }
+    }
+    free(sh);
+    free(sw);
+    free(sc);
+  }
+}
+
+/* Gradient with respect to the weights (C x K). */
+void oracle_bwd_weight_ex(const double* x, const double* dy, const double* theta_deg, double* dwt,
+                          int N, int C, int H, int W, int K, int str, int mode, int nthreads) {
+  const int P = oracle_out_size(H, str), Q = oracle_out_size(W, str);
+#pragma omp parallel for schedule(dynamic) num_threads(nthreads)
+  for (int c = 0; c < C; ++c) {
+    int* sh = (int*)malloc(sizeof(int) * 4 * (size_t)K);
+    int* sw = (int*)malloc(sizeof(int) * 4 * (size_t)K);
+    double* sc = (double*)malloc(sizeof(double) * 4 * (size_t)K);
+    tap_samples(theta_deg[c], K, mode, sh, sw, sc);
+    double* g = dwt + (size_t)c * K;
+    for (int k = 0; k < K; ++k) g[k] = 0.0;
+    for (int n = 0; n < N; ++n) {
+      const double* xp = x + ((size_t)n * C + c) * H * W;
+      const double* gp = dy + ((size_t)n * C + c) * P * Q;
+      for (int p = 0; p < P; ++p) {
+        for (int q = 0; q < Q; ++q) {
+          const double gy = gp[(size_t)p * Q + q];
+          for (int k = 0; k < K; ++k) {
+            for (int s = 0; s < 4; ++s) {
+              if (sc[4 * k + s] == 0.0) continue;
+              const int h = str * p + sh[4 * k + s];
+              const int w = str * q + sw[4 * k + s];
+              if (h >= 0 && h < H && w >= 0 && w < W) g[k] += gy * sc[4 * k + s] * xp[(size_t)h * W + w];
+            }
+          }
+        }
+      }
+    }
+    free(sh);
+    free(sw);
+    free(sc);
+  }
+}
