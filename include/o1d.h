@@ -58,10 +58,26 @@ typedef enum {
 } o1d_dtype_t;
 
 typedef enum {
+  O1D_NCHW = 0, /* x[n][c][h][w] */
+  O1D_NHWC = 1  /* x[n][h][w][c], Definition 1's own layout */
+} o1d_layout_t;
+
+typedef enum {
+  O1D_FLOOR = 0,   /* Eq. (2): offsets rounded down */
+  O1D_BILINEAR = 1 /* bilinear interpolation at the unrounded offsets (section "Discretization and
+                      Interpolation"): tap k reads the four pixels around (str p + rh_k, str q + rw_k),
+                      (rh_k, rw_k) = (-(k - K/2) sin theta, (k - K/2) cos theta), weighted by
+                      (1-fh)(1-fw), (1-fh)fw, fh(1-fw), fh fw with fh, fw the fractional parts
+                      (a part within 1e-9 of 0 or 1 is taken as 0 with the integer moved accordingly) */
+} o1d_sampling_t;
+
+typedef enum {
   O1D_OK = 0,
   O1D_ERR_INVALID = 1,     /* NULL pointer for a non-empty tensor, negative size, even or non-positive K,
                               unknown dtype, aliasing output */
-  O1D_ERR_UNSUPPORTED = 2, /* K above O1D_MAX_K, or a size beyond the kernels' 32-bit index range */
+  O1D_ERR_UNSUPPORTED = 2, /* K above O1D_MAX_K, a stride above 64, a size beyond the kernels' 32-bit index
+                              range (2^31 elements, 65535 images or channels), or a zero-margined band of the
+                              plane too large for LDS */
   O1D_ERR_WORKSPACE = 3,   /* workspace smaller than o1d_bwd_weight_workspace_bytes() */
   O1D_ERR_HIP = 4          /* the HIP runtime rejected a kernel launch */
 } o1d_status_t;
@@ -107,6 +123,57 @@ o1d_status_t o1d_bwd(const void* x, const void* dy, const void* w, const float* 
 
 /* Workspace size in bytes that o1d_bwd_weight (and o1d_bwd) needs for these sizes. */
 size_t o1d_bwd_weight_workspace_bytes(int N, int C, int H, int W, int K, o1d_dtype_t dtype);
+
+/* ---- Stride, layout and sampling (Definition 1 with its stride `str`, Eq. 2).
+ *
+ * The _ex entry points compute the same three operations for any stride >= 1
+ * (at most 64), either memory layout and either discretisation.  The input
+ * plane is H x W; the output plane is P x Q with P = (H - 1) / stride + 1 and
+ * Q = (W - 1) / stride + 1 (integer division: output (p, q) is centred on
+ * input (stride p, stride q)):
+ *   y[n,c,p,q]  = sum_k w[c,k] sample_k(x[n,c], stride p, stride q)
+ *   dx[n,c,h,w] = the adjoint of that map in x (a scatter of dy, computed as a gather)
+ *   dw[c,k]     = sum_{n,p,q} dy[n,c,p,q] sample_k(x[n,c], stride p, stride q)
+ * where sample_k reads the pixel at the rounded-down offsets of Eq. (2)
+ * (O1D_FLOOR) or interpolates bilinearly at the unrounded ones (O1D_BILINEAR),
+ * pixels outside the plane reading zero.  Layouts: x and dx are N x C x H x W
+ * (O1D_NCHW) or N x H x W x C (O1D_NHWC); y and dy are N x C x P x Q or
+ * N x P x Q x C; w, dw are [C][K]; theta_deg is [C].  With stride 1, O1D_NCHW
+ * and O1D_FLOOR they are exactly o1d_fwd, o1d_bwd_input and o1d_bwd_weight.
+ * Ownership, asynchrony, precision, error and empty-tensor rules are those of
+ * the plain entry points; H and W are always the input plane's, also for
+ * o1d_bwd_input_ex.  O1D_ERR_UNSUPPORTED is returned where a band of the
+ * plane with its zero margin does not fit in LDS (K and stride both very
+ * large).  The weight gradient's workspace is
+ * o1d_bwd_weight_ex_workspace_bytes(...) bytes. */
+o1d_status_t o1d_fwd_ex(const void* x, const void* w, const float* theta_deg, void* y,
+                        int N, int C, int H, int W, int K, int stride, o1d_layout_t layout,
+                        o1d_sampling_t sampling, o1d_dtype_t dtype, void* stream);
+o1d_status_t o1d_bwd_input_ex(const void* dy, const void* w, const float* theta_deg, void* dx,
+                              int N, int C, int H, int W, int K, int stride, o1d_layout_t layout,
+                              o1d_sampling_t sampling, o1d_dtype_t dtype, void* stream);
+o1d_status_t o1d_bwd_weight_ex(const void* x, const void* dy, const float* theta_deg, void* dw,
+                               int N, int C, int H, int W, int K, int stride, o1d_layout_t layout,
+                               o1d_sampling_t sampling, o1d_dtype_t dtype,
+                               void* workspace, size_t workspace_bytes, void* stream);
+size_t o1d_bwd_weight_ex_workspace_bytes(int N, int C, int H, int W, int K, int stride, o1d_layout_t layout,
+                                         o1d_sampling_t sampling, o1d_dtype_t dtype);
+
+/* ---- Planning introspection (host only, no device work; for tests and tools).
+ *
+ * o1d_kernel_name: the kernel(s) a call with these arguments would launch,
+ * e.g. "strip_gather/f32/S87/KB32" or "gen_wgrad/bf16/nhwc/RP4"; two names
+ * joined by '+' where o1d_bwd runs the input and weight gradients in turn.
+ * op: 0 = o1d_fwd(_ex), 1 = o1d_bwd_input(_ex), 2 = o1d_bwd_weight(_ex),
+ * 3 = o1d_bwd (stride 1, NCHW, O1D_FLOOR only).  `aligned` != 0 states that
+ * the tensors are 16-byte (O1D_F32) or 8-byte (O1D_BF16) aligned.  Returns ""
+ * for invalid or empty sizes.  The string lives in thread-local storage until
+ * the thread's next call.
+ * o1d_kernel_variant: the i-th kernel instantiation compiled into the
+ * library, in the same naming, or NULL for i past the last. */
+const char* o1d_kernel_name(int op, int N, int C, int H, int W, int K, int stride, o1d_layout_t layout,
+                            o1d_sampling_t sampling, o1d_dtype_t dtype, int aligned);
+const char* o1d_kernel_variant(int i);
 
 /* Static description of a status code. */
 const char* o1d_status_str(o1d_status_t status);

@@ -2,13 +2,15 @@
 
 Usage: ``python -m paper_2309_15812_amd.build`` (or ``build()`` from Python).
 Cross-compiles without a GPU.  Every ``csrc/*.hip`` translation unit is
-compiled to an object in parallel (the line kernels are split per storage
-type and kind for this), then the objects are linked into the library.
+compiled to an object in parallel (the strip kernels are split per family,
+storage type and cell bound for this), then the objects are linked into the
+library.
 """
 from __future__ import annotations
 
 import concurrent.futures
 import glob
+import hashlib
 import os
 import shutil
 import subprocess
@@ -37,12 +39,12 @@ def sources() -> list[str]:
     return sorted(glob.glob(os.path.join(CSRC, "*.hip")))
 
 
-# The line kernels keep LDS reads in flight across inline-assembly blocks in
-# registers the compiler believes are written; a register spill between two
-# such blocks would store a value before it arrives.  Their translation units
-# are therefore compiled with resource remarks and rejected if any kernel in
-# them uses scratch memory.
-CHECKED = ("o1d_line_", "o1d_strip_")
+# The strip kernels are sized to stay in registers (their walks keep a
+# window and per-output accumulators of up to 60 values per lane); a spill to
+# scratch memory would cost far more than it saves, so their translation
+# units are compiled with resource remarks and rejected if any kernel in them
+# uses scratch memory.  The general kernels are checked the same way.
+CHECKED = ("o1d_strip_", "o1d_gen_")
 REMARK = "-Rpass-analysis=kernel-resource-usage"
 
 
@@ -69,17 +71,42 @@ def _run(cmd: list[str], verbose: bool) -> None:
         _check_no_scratch(cmd[-1], res.stderr)
 
 
-def build(verbose: bool = False, jobs: int | None = None) -> str:
+def _key(src: str, flags: list[str]) -> str:
+    """Hash of a translation unit, every header it may include and the flags."""
+    h = hashlib.sha256(" ".join(flags).encode())
+    for f in [src, *sorted(glob.glob(os.path.join(CSRC, "*.h"))), os.path.join(INCLUDE, "o1d.h")]:
+        with open(f, "rb") as fh:
+            h.update(os.path.basename(f).encode() + b"\0" + fh.read())
+    return h.hexdigest()[:20]
+
+
+def build(verbose: bool = False, jobs: int | None = None, incremental: bool = False) -> str:
+    """Compiles every translation unit and links libo1d.so.  With incremental=True, objects whose source,
+    headers and flags are unchanged are reused from _build/ (a development aid; the default always
+    recompiles everything)."""
     srcs = sources()
     jobs = jobs or min(len(srcs), max(1, min(os.cpu_count() or 1, 16)))
     tmpdir = tempfile.mkdtemp(prefix="o1d_build_")
+    cache = os.path.join(PKG, "_build")
     try:
-        objs = [os.path.join(tmpdir, os.path.basename(s) + ".o") for s in srcs]
-        cmds = [[HIPCC, *FLAGS, *([REMARK] if os.path.basename(s).startswith(CHECKED) else []),
-                 "-I", INCLUDE, "-I", CSRC, "-c", "-o", o, s] for s, o in zip(srcs, objs)]
+        objs, cmds = [], []
+        for src in srcs:
+            extra = [REMARK] if os.path.basename(src).startswith(CHECKED) else []
+            flags = [*FLAGS, *extra]
+            obj = os.path.join(tmpdir, os.path.basename(src) + ".o")
+            cached = os.path.join(cache, os.path.basename(src) + "." + _key(src, flags) + ".o")
+            if incremental and os.path.exists(cached):
+                shutil.copy(cached, obj)
+            else:
+                cmds.append(([HIPCC, *flags, "-I", INCLUDE, "-I", CSRC, "-c", "-o", obj, src], obj, cached))
+            objs.append(obj)
         with concurrent.futures.ThreadPoolExecutor(max_workers=jobs) as ex:
-            for fut in [ex.submit(_run, c, verbose) for c in cmds]:
+            for fut in [ex.submit(_run, c, verbose) for c, _, _ in cmds]:
                 fut.result()
+        if incremental:
+            os.makedirs(cache, exist_ok=True)
+            for _, obj, cached in cmds:
+                shutil.copy(obj, cached)
         tmp = LIB + ".tmp"
         _run([HIPCC, "--offload-arch=gfx950", "-shared", "-fPIC", "-o", tmp, *objs], verbose)
         os.replace(tmp, LIB)
@@ -89,4 +116,4 @@ def build(verbose: bool = False, jobs: int | None = None) -> str:
 
 
 if __name__ == "__main__":
-    print(build(verbose=True))
+    print(build(verbose=True, incremental="--incremental" in sys.argv))

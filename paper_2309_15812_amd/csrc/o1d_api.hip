@@ -1,21 +1,29 @@
 // C ABI of the oriented 1D depthwise convolution library (declared in
-// include/o1d.h): argument validation, status codes, per-thread error text
-// and dispatch to the kernel launchers.  No device memory is allocated here.
+// include/o1d.h): argument validation, status codes, per-thread error text,
+// the choice of kernel family and dispatch to the launchers.  No device
+// memory is allocated here.
+//
+// Kernel families:
+//  * strip kernels (o1d_strip*.h): NCHW, stride 1, offsets rounded down,
+//    W a multiple of 4, vector-aligned tensors, planes whose zero-margined
+//    tile fits the compiled tile strides; gathers for K <= 63, the weight
+//    gradient and the fused backward for K <= 31;
+//  * general kernels (o1d_gen*.h): everything else the ABI accepts.
 #include <hip/hip_runtime.h>
 #include <stdarg.h>
 #include <stdint.h>
 #include <stdio.h>
-#include <stdlib.h>
+#include <string.h>
 
 #include "o1d.h"
+#include "o1d_gen.h"
 #include "o1d_launch.h"
-#include "o1d_plan.h"
-#include "o1d_line.h"
 #include "o1d_strip.h"
 
 namespace {
 
 thread_local char g_last_error[512] = "";
+thread_local char g_name[256] = "";
 
 o1d_status_t fail(o1d_status_t st, const char* fmt, ...) {
   va_list ap;
@@ -31,66 +39,94 @@ o1d_status_t ok() {
 }
 
 size_t elem_size(o1d_dtype_t dt) { return dt == O1D_BF16 ? 2u : 4u; }
+const char* dt_name(o1d_dtype_t dt) { return dt == O1D_BF16 ? "bf16" : "f32"; }
 
 bool overlaps(const void* a, size_t abytes, const void* b, size_t bbytes) {
   const uintptr_t a0 = (uintptr_t)a, b0 = (uintptr_t)b;
   return a0 < b0 + bbytes && b0 < a0 + abytes;
 }
 
-// Checks shared by all entry points.  Sets *empty when there is nothing to
-// compute over the batch/plane (N, H or W zero) or no channel (C zero).
-o1d_status_t check_sizes(const char* fn, int N, int C, int H, int W, int K, o1d_dtype_t dt) {
+// The options every entry point takes (the plain entry points: stride 1,
+// NCHW, rounding down).
+struct Opts {
+  int stride = 1;
+  o1d_layout_t layout = O1D_NCHW;
+  o1d_sampling_t sampling = O1D_FLOOR;
+  bool plain() const { return stride == 1 && layout == O1D_NCHW && sampling == O1D_FLOOR; }
+};
+
+// Checks shared by all entry points.
+o1d_status_t check_sizes(const char* fn, int N, int C, int H, int W, int K, o1d_dtype_t dt, const Opts& o) {
   if (dt != O1D_F32 && dt != O1D_BF16) return fail(O1D_ERR_INVALID, "%s: unknown dtype %d", fn, (int)dt);
   if (N < 0 || C < 0 || H < 0 || W < 0)
     return fail(O1D_ERR_INVALID, "%s: negative size N=%d C=%d H=%d W=%d", fn, N, C, H, W);
   if (K < 1 || (K % 2) == 0)
     return fail(O1D_ERR_INVALID, "%s: K=%d must be odd and positive (pad = K/2 centres the kernel)", fn, K);
+  if (o.stride < 1) return fail(O1D_ERR_INVALID, "%s: stride %d must be >= 1", fn, o.stride);
+  if (o.layout != O1D_NCHW && o.layout != O1D_NHWC)
+    return fail(O1D_ERR_INVALID, "%s: unknown layout %d", fn, (int)o.layout);
+  if (o.sampling != O1D_FLOOR && o.sampling != O1D_BILINEAR)
+    return fail(O1D_ERR_INVALID, "%s: unknown sampling %d", fn, (int)o.sampling);
   if (K > O1D_MAX_K) return fail(O1D_ERR_UNSUPPORTED, "%s: K=%d exceeds O1D_MAX_K=%d", fn, K, O1D_MAX_K);
+  if (o.stride > 64) return fail(O1D_ERR_UNSUPPORTED, "%s: stride %d exceeds 64", fn, o.stride);
   if (C > 65535 || N > 65535)
     return fail(O1D_ERR_UNSUPPORTED, "%s: N=%d or C=%d exceeds the 65535 grid limit", fn, N, C);
-  if ((long long)H * (long long)W > (1ll << 30))
-    return fail(O1D_ERR_UNSUPPORTED, "%s: plane %dx%d exceeds 2^30 elements", fn, H, W);
+  if ((long long)N * C * (long long)H * W >= (1ll << 31))
+    return fail(O1D_ERR_UNSUPPORTED, "%s: %d x %d x %d x %d elements exceed 2^31", fn, N, C, H, W);
   return O1D_OK;
-}
-
-// Kernel family: the line kernels cover K <= 63, planes up to 64 columns and
-// haloed tiles that fit in LDS; everything else takes the general tiled
-// kernels.  O1D_KERNEL=tiled forces the tiled kernels (a comparison aid).
-bool line_allowed() {
-  const char* e = getenv("O1D_KERNEL");
-  return !(e && e[0] == 't');
-}
-
-o1d::line::LinePlan line_plan(int N, int C, int H, int W, int K, int sign, int kind, bool vec_ok) {
-  if (!line_allowed()) return o1d::line::LinePlan();
-  return o1d::line::plan_line(N, C, H, W, K, sign, kind, vec_ok);
 }
 
 // Vector staging needs 16-byte (float32) or 8-byte (bfloat16) aligned tensors.
 bool vec_aligned(const void* p, o1d_dtype_t dt) { return ((uintptr_t)p % (dt == O1D_BF16 ? 8u : 16u)) == 0; }
 
-// The workspace size must not depend on pointer alignment: take the larger
-// partial count of the kernels that aligned and unaligned tensors select
-// (the line kernels need aligned tensors; otherwise the tiled kernels run).
-o1d::strip::Plan strip_wgrad_plan(int N, int C, int H, int W, int K, bool vec_ok) {
-  if (!line_allowed()) return o1d::strip::Plan();
-  return o1d::strip::plan_strip(N, C, H, W, K, 1, 1, vec_ok);
+enum OpKind { kOpFwd = 0, kOpDgrad = 1, kOpWgrad = 2, kOpBwd = 3 };
+
+// The kernels one op runs.  For the fused backward (kOpBwd) the route is ok
+// only where the fused strip kernel applies (its plan in `sp`); otherwise
+// o1d_bwd runs the input gradient's route and then the weight gradient's.
+struct Route {
+  bool ok = false;
+  bool use_strip = false;
+  o1d::strip::Plan sp;
+  o1d::gen::Plan gp;
+};
+
+Route route(int op, int N, int C, int H, int W, int K, o1d_dtype_t dt, const Opts& o, bool aligned) {
+  Route r;
+  if (o.plain() && op != kOpBwd) {
+    r.sp = o1d::strip::plan_strip(N, C, H, W, K, op == kOpDgrad ? -1 : 1, op == kOpWgrad ? 1 : 0, aligned);
+    if (r.sp.ok) {
+      r.ok = r.use_strip = true;
+      return r;
+    }
+  }
+  if (op == kOpBwd) {
+    if (o.plain()) {
+      r.sp = o1d::strip::plan_strip(N, C, H, W, K, -1, 1, aligned);
+      if (r.sp.ok) r.ok = r.use_strip = true;
+    }
+    return r;  // otherwise: not ok, the two separate routes run
+  }
+  const int gop = op == kOpFwd ? o1d::gen::kFwd : (op == kOpDgrad ? o1d::gen::kDgrad : o1d::gen::kWgrad);
+  r.gp = o1d::gen::plan_gen(gop, o.layout == O1D_NHWC ? o1d::gen::kNHWC : o1d::gen::kNCHW, N, C, H, W, K, o.stride,
+                            o.sampling == O1D_BILINEAR ? 1 : 0, (int)elem_size(dt));
+  r.ok = r.gp.ok;
+  return r;
 }
 
-size_t wgrad_workspace(int N, int C, int H, int W, int K) {
-  const o1d::strip::Plan sa = strip_wgrad_plan(N, C, H, W, K, true);
-  if (sa.ok) {
-    // aligned tensors take the strip kernel, unaligned ones a line or tiled kernel
-    const o1d::line::LinePlan b = line_plan(N, C, H, W, K, 1, 1, false);
-    const size_t pb = b.ok ? (size_t)b.blocks_n : o1d::plan_wgrad(N, C, H, W, K).parts();
-    const size_t parts = (size_t)sa.blocks_n > pb ? (size_t)sa.blocks_n : pb;
-    return parts * (size_t)C * (size_t)K * sizeof(float);
+// Partial rows per channel of the weight gradient's route.
+size_t route_parts(const Route& r) { return r.use_strip ? (size_t)r.sp.blocks_n : r.gp.parts; }
+
+// The weight gradient's workspace holds one partial row of K float32 per
+// channel and workgroup.  Its size must not depend on pointer alignment, so
+// the larger partial count of the aligned and unaligned routes is reported
+// (the fused backward's strip plan has the weight gradient's partial count).
+size_t wgrad_workspace(int N, int C, int H, int W, int K, o1d_dtype_t dt, const Opts& o) {
+  size_t parts = 0;
+  for (int a = 0; a < 2; ++a) {
+    const Route r = route(kOpWgrad, N, C, H, W, K, dt, o, a != 0);
+    if (r.ok && route_parts(r) > parts) parts = route_parts(r);
   }
-  const o1d::line::LinePlan a = line_plan(N, C, H, W, K, 1, 1, true);
-  const o1d::line::LinePlan b = line_plan(N, C, H, W, K, 1, 1, false);
-  const size_t tiled = o1d::plan_wgrad(N, C, H, W, K).parts();
-  const size_t pa = a.ok ? (size_t)a.blocks_n : tiled, pb = b.ok ? (size_t)b.blocks_n : tiled;
-  const size_t parts = pa > pb ? pa : pb;
   return parts * (size_t)C * (size_t)K * sizeof(float);
 }
 
@@ -99,102 +135,95 @@ o1d_status_t hip_status(const char* fn, hipError_t e) {
   return ok();
 }
 
+o1d_status_t unsupported(const char* fn, int N, int C, int H, int W, int K) {
+  return fail(O1D_ERR_UNSUPPORTED, "%s: no kernel covers N=%d C=%d H=%d W=%d K=%d (LDS tile too large)", fn, N, C, H,
+              W, K);
+}
+
+// Tensor sizes of the op's tensors in elements: input plane and output plane.
+size_t in_elems(int N, int C, int H, int W) { return (size_t)N * C * H * W; }
+size_t out_elems(int N, int C, int H, int W, int s) {
+  return (size_t)N * C * (size_t)o1d::gen::out_size(H, s) * (size_t)o1d::gen::out_size(W, s);
+}
+
+// Forward (sign +1: x -> y) or input gradient (sign -1: dy -> dx) after the
+// size checks.  H and W are always the input plane's.
 o1d_status_t gather_entry(const char* fn, const void* in, const void* w, const float* theta, void* out, int N, int C,
-                          int H, int W, int K, o1d_dtype_t dt, void* stream, int sign) {
-  o1d_status_t st = check_sizes(fn, N, C, H, W, K, dt);
+                          int H, int W, int K, o1d_dtype_t dt, const Opts& o, void* stream, int sign) {
+  o1d_status_t st = check_sizes(fn, N, C, H, W, K, dt, o);
   if (st != O1D_OK) return st;
-  const size_t elems = (size_t)N * C * H * W;
-  if (elems == 0) return ok();
+  if (in_elems(N, C, H, W) == 0) return ok();
   if (!in || !w || !theta || !out) return fail(O1D_ERR_INVALID, "%s: NULL tensor pointer", fn);
-  const size_t bytes = elems * elem_size(dt);
-  if (overlaps(in, bytes, out, bytes)) return fail(O1D_ERR_INVALID, "%s: output overlaps input", fn);
+  const size_t xb = in_elems(N, C, H, W) * elem_size(dt), yb = out_elems(N, C, H, W, o.stride) * elem_size(dt);
+  const size_t inb = sign > 0 ? xb : yb, outb = sign > 0 ? yb : xb;
+  if (overlaps(in, inb, out, outb)) return fail(O1D_ERR_INVALID, "%s: output overlaps input", fn);
   (void)hipGetLastError();
   hipStream_t s = static_cast<hipStream_t>(stream);
   const bool va = vec_aligned(in, dt) && vec_aligned(out, dt);
-  if (line_allowed()) {
-    const o1d::strip::Plan sp = o1d::strip::plan_strip(N, C, H, W, K, sign, 0, va);
-    if (sp.ok) return hip_status(fn, o1d::launch_gather_strip((o1d::Dtype)dt, sp, in, w, theta, out, s));
-  }
-  const o1d::line::LinePlan lp = line_plan(N, C, H, W, K, sign, 0, va);
-  if (lp.ok) return hip_status(fn, o1d::launch_gather_line((o1d::Dtype)dt, lp, in, w, theta, out, s));
-  return hip_status(fn, o1d::launch_gather((o1d::Dtype)dt, in, w, theta, out, N, C, H, W, K, sign, s));
+  const Route r = route(sign > 0 ? kOpFwd : kOpDgrad, N, C, H, W, K, dt, o, va);
+  if (!r.ok) return unsupported(fn, N, C, H, W, K);
+  if (r.use_strip) return hip_status(fn, o1d::launch_gather_strip((o1d::Dtype)dt, r.sp, in, w, theta, out, s));
+  return hip_status(fn, o1d::launch_gen_gather((o1d::Dtype)dt, r.gp, (int)o.layout, in, w, theta, out, s));
 }
 
-// Weight gradient after validation: the strip kernel, else a line kernel,
-// else the tiled kernels (the workspace covers all three, see above).
+// Weight gradient after validation.
 o1d_status_t wgrad_dispatch(const char* fn, const void* x, const void* dy, const float* theta, void* dw, int N, int C,
-                            int H, int W, int K, o1d_dtype_t dt, void* workspace, hipStream_t s) {
+                            int H, int W, int K, o1d_dtype_t dt, const Opts& o, void* workspace, hipStream_t s) {
   const bool va = vec_aligned(x, dt) && vec_aligned(dy, dt);
-  const o1d::strip::Plan sp = strip_wgrad_plan(N, C, H, W, K, va);
-  if (sp.ok)
-    return hip_status(fn, o1d::launch_wgrad_strip((o1d::Dtype)dt, sp, x, dy, theta, dw,
-                                                  static_cast<float*>(workspace), s));
-  const o1d::line::LinePlan lp = line_plan(N, C, H, W, K, 1, 1, va);
-  if (lp.ok)
-    return hip_status(fn, o1d::launch_wgrad_line((o1d::Dtype)dt, lp, x, dy, theta, dw,
-                                                 static_cast<float*>(workspace), s));
-  return hip_status(fn, o1d::launch_wgrad((o1d::Dtype)dt, x, dy, theta, dw, static_cast<float*>(workspace), N, C, H,
-                                          W, K, s));
+  const Route r = route(kOpWgrad, N, C, H, W, K, dt, o, va);
+  if (!r.ok) return unsupported(fn, N, C, H, W, K);
+  float* part = static_cast<float*>(workspace);
+  if (r.use_strip) return hip_status(fn, o1d::launch_wgrad_strip((o1d::Dtype)dt, r.sp, x, dy, theta, dw, part, s));
+  return hip_status(fn, o1d::launch_gen_wgrad((o1d::Dtype)dt, r.gp, (int)o.layout, x, dy, theta, dw, part, s));
 }
 
-}  // namespace
-
-extern "C" {
-
-size_t o1d_bwd_weight_workspace_bytes(int N, int C, int H, int W, int K, o1d_dtype_t dtype) {
-  if (check_sizes("o1d_bwd_weight_workspace_bytes", N, C, H, W, K, dtype) != O1D_OK) return 0;
-  if ((size_t)N * C * H * W == 0) return 0;
-  return wgrad_workspace(N, C, H, W, K);
-}
-
-o1d_status_t o1d_fwd(const void* x, const void* w, const float* theta_deg, void* y, int N, int C, int H, int W, int K,
-                     o1d_dtype_t dtype, void* stream) {
-  return gather_entry("o1d_fwd", x, w, theta_deg, y, N, C, H, W, K, dtype, stream, +1);
-}
-
-o1d_status_t o1d_bwd_input(const void* dy, const void* w, const float* theta_deg, void* dx, int N, int C, int H,
-                           int W, int K, o1d_dtype_t dtype, void* stream) {
-  return gather_entry("o1d_bwd_input", dy, w, theta_deg, dx, N, C, H, W, K, dtype, stream, -1);
-}
-
-o1d_status_t o1d_bwd_weight(const void* x, const void* dy, const float* theta_deg, void* dw, int N, int C, int H,
-                            int W, int K, o1d_dtype_t dtype, void* workspace, size_t workspace_bytes, void* stream) {
-  const char* fn = "o1d_bwd_weight";
-  o1d_status_t st = check_sizes(fn, N, C, H, W, K, dtype);
+o1d_status_t bwd_weight_entry(const char* fn, const void* x, const void* dy, const float* theta_deg, void* dw, int N,
+                              int C, int H, int W, int K, o1d_dtype_t dtype, const Opts& o, void* workspace,
+                              size_t workspace_bytes, void* stream) {
+  o1d_status_t st = check_sizes(fn, N, C, H, W, K, dtype, o);
   if (st != O1D_OK) return st;
   if (C == 0) return ok();
   if (!dw) return fail(O1D_ERR_INVALID, "%s: NULL dw pointer", fn);
   hipStream_t s = static_cast<hipStream_t>(stream);
-  const size_t elems = (size_t)N * C * H * W;
   (void)hipGetLastError();
-  if (elems == 0) return hip_status(fn, o1d::launch_zero((o1d::Dtype)dtype, dw, (size_t)C * K, s));
+  if (in_elems(N, C, H, W) == 0) return hip_status(fn, o1d::launch_zero((o1d::Dtype)dtype, dw, (size_t)C * K, s));
   if (!x || !dy || !theta_deg) return fail(O1D_ERR_INVALID, "%s: NULL tensor pointer", fn);
-  const size_t need = o1d_bwd_weight_workspace_bytes(N, C, H, W, K, dtype);
-  if (workspace_bytes < need || (need > 0 && !workspace))
+  const size_t need = wgrad_workspace(N, C, H, W, K, dtype, o);
+  if (need == 0) return unsupported(fn, N, C, H, W, K);
+  if (workspace_bytes < need || !workspace)
     return fail(O1D_ERR_WORKSPACE, "%s: workspace of %zu bytes given, %zu needed", fn, workspace_bytes, need);
-  const size_t dwbytes = (size_t)C * K * elem_size(dtype), tbytes = elems * elem_size(dtype);
-  if (overlaps(dw, dwbytes, x, tbytes) || overlaps(dw, dwbytes, dy, tbytes) ||
-      (need > 0 && (overlaps(workspace, need, x, tbytes) || overlaps(workspace, need, dy, tbytes) ||
-                    overlaps(workspace, need, dw, dwbytes))))
+  const size_t dwb = (size_t)C * K * elem_size(dtype), xb = in_elems(N, C, H, W) * elem_size(dtype);
+  const size_t yb = out_elems(N, C, H, W, o.stride) * elem_size(dtype);
+  if (overlaps(dw, dwb, x, xb) || overlaps(dw, dwb, dy, yb) || overlaps(workspace, need, x, xb) ||
+      overlaps(workspace, need, dy, yb) || overlaps(workspace, need, dw, dwb))
     return fail(O1D_ERR_INVALID, "%s: dw or workspace overlaps an input", fn);
-  return wgrad_dispatch(fn, x, dy, theta_deg, dw, N, C, H, W, K, dtype, workspace, s);
+  return wgrad_dispatch(fn, x, dy, theta_deg, dw, N, C, H, W, K, dtype, o, workspace, s);
 }
 
-o1d_status_t o1d_bwd(const void* x, const void* dy, const void* w, const float* theta_deg, void* dx, void* dw, int N,
-                     int C, int H, int W, int K, o1d_dtype_t dtype, void* workspace, size_t workspace_bytes,
-                     void* stream) {
-  const char* fn = "o1d_bwd";
-  o1d_status_t st = check_sizes(fn, N, C, H, W, K, dtype);
+void name_of(char* buf, size_t n, int op, const Route& r, o1d_dtype_t dt, const Opts& o) {
+  static const char* fam[] = {"gather", "gather", "wgrad", "bwd"};
+  if (r.use_strip)
+    snprintf(buf, n, "strip_%s/%s/S%d/KB%d", fam[op], dt_name(dt), r.sp.S, r.sp.KB);
+  else
+    snprintf(buf, n, "gen_%s/%s/%s/RP%d", fam[op], dt_name(dt), o.layout == O1D_NHWC ? "nhwc" : "nchw", r.gp.p.RP);
+}
+
+o1d_status_t bwd_entry(const char* fn, const void* x, const void* dy, const void* w, const float* theta_deg,
+                       void* dx, void* dw, int N, int C, int H, int W, int K, o1d_dtype_t dtype, void* workspace,
+                       size_t workspace_bytes, void* stream) {
+  const Opts o;
+  o1d_status_t st = check_sizes(fn, N, C, H, W, K, dtype, o);
   if (st != O1D_OK) return st;
   if (C == 0) return ok();
   if (!dw) return fail(O1D_ERR_INVALID, "%s: NULL dw pointer", fn);
   hipStream_t s = static_cast<hipStream_t>(stream);
-  const size_t elems = (size_t)N * C * H * W;
+  const size_t elems = in_elems(N, C, H, W);
   (void)hipGetLastError();
   if (elems == 0) return hip_status(fn, o1d::launch_zero((o1d::Dtype)dtype, dw, (size_t)C * K, s));
   if (!x || !dy || !w || !theta_deg || !dx) return fail(O1D_ERR_INVALID, "%s: NULL tensor pointer", fn);
-  const size_t need = o1d_bwd_weight_workspace_bytes(N, C, H, W, K, dtype);
-  if (workspace_bytes < need || (need > 0 && !workspace))
+  const size_t need = wgrad_workspace(N, C, H, W, K, dtype, o);
+  if (need == 0) return unsupported(fn, N, C, H, W, K);
+  if (workspace_bytes < need || !workspace)
     return fail(O1D_ERR_WORKSPACE, "%s: workspace of %zu bytes given, %zu needed", fn, workspace_bytes, need);
   const size_t wbytes = (size_t)C * K * elem_size(dtype), tbytes = elems * elem_size(dtype);
   if (overlaps(dx, tbytes, x, tbytes) || overlaps(dx, tbytes, dy, tbytes) || overlaps(dx, tbytes, w, wbytes))
@@ -202,21 +231,145 @@ o1d_status_t o1d_bwd(const void* x, const void* dy, const void* w, const float* 
   if (overlaps(dw, wbytes, x, tbytes) || overlaps(dw, wbytes, dy, tbytes) || overlaps(dw, wbytes, w, wbytes) ||
       overlaps(dw, wbytes, dx, tbytes))
     return fail(O1D_ERR_INVALID, "%s: dw overlaps an input or dx", fn);
-  if (need > 0 && (overlaps(workspace, need, x, tbytes) || overlaps(workspace, need, dy, tbytes) ||
-                   overlaps(workspace, need, w, wbytes) || overlaps(workspace, need, dx, tbytes) ||
-                   overlaps(workspace, need, dw, wbytes)))
+  if (overlaps(workspace, need, x, tbytes) || overlaps(workspace, need, dy, tbytes) ||
+      overlaps(workspace, need, w, wbytes) || overlaps(workspace, need, dx, tbytes) ||
+      overlaps(workspace, need, dw, wbytes))
     return fail(O1D_ERR_INVALID, "%s: workspace overlaps a tensor", fn);
   const bool va = vec_aligned(x, dtype) && vec_aligned(dy, dtype) && vec_aligned(dx, dtype);
-  if (line_allowed()) {
-    // the weight gradient's plan (hence its workspace) with mirrored offsets
-    o1d::strip::Plan sp = o1d::strip::plan_strip(N, C, H, W, K, -1, 1, va);
-    if (sp.ok)
-      return hip_status(fn, o1d::launch_bwd_strip((o1d::Dtype)dtype, sp, x, dy, w, theta_deg, dx, dw,
-                                                  static_cast<float*>(workspace), s));
-  }
-  st = gather_entry(fn, dy, w, theta_deg, dx, N, C, H, W, K, dtype, stream, -1);
+  const Route r = route(kOpBwd, N, C, H, W, K, dtype, o, va);
+  if (r.ok)
+    return hip_status(fn, o1d::launch_bwd_strip((o1d::Dtype)dtype, r.sp, x, dy, w, theta_deg, dx, dw,
+                                                static_cast<float*>(workspace), s));
+  st = gather_entry(fn, dy, w, theta_deg, dx, N, C, H, W, K, dtype, o, stream, -1);
   if (st != O1D_OK) return st;
-  return wgrad_dispatch(fn, x, dy, theta_deg, dw, N, C, H, W, K, dtype, workspace, s);
+  return wgrad_dispatch(fn, x, dy, theta_deg, dw, N, C, H, W, K, dtype, o, workspace, s);
+}
+
+
+}  // namespace
+
+extern "C" {
+
+size_t o1d_bwd_weight_workspace_bytes(int N, int C, int H, int W, int K, o1d_dtype_t dtype) {
+  const Opts o;
+  if (check_sizes("o1d_bwd_weight_workspace_bytes", N, C, H, W, K, dtype, o) != O1D_OK) return 0;
+  if (in_elems(N, C, H, W) == 0) return 0;
+  return wgrad_workspace(N, C, H, W, K, dtype, o);
+}
+
+size_t o1d_bwd_weight_ex_workspace_bytes(int N, int C, int H, int W, int K, int stride, o1d_layout_t layout,
+                                         o1d_sampling_t sampling, o1d_dtype_t dtype) {
+  Opts o;
+  o.stride = stride;
+  o.layout = layout;
+  o.sampling = sampling;
+  if (check_sizes("o1d_bwd_weight_ex_workspace_bytes", N, C, H, W, K, dtype, o) != O1D_OK) return 0;
+  if (in_elems(N, C, H, W) == 0) return 0;
+  return wgrad_workspace(N, C, H, W, K, dtype, o);
+}
+
+o1d_status_t o1d_fwd(const void* x, const void* w, const float* theta_deg, void* y, int N, int C, int H, int W, int K,
+                     o1d_dtype_t dtype, void* stream) {
+  return gather_entry("o1d_fwd", x, w, theta_deg, y, N, C, H, W, K, dtype, Opts(), stream, +1);
+}
+
+o1d_status_t o1d_bwd_input(const void* dy, const void* w, const float* theta_deg, void* dx, int N, int C, int H,
+                           int W, int K, o1d_dtype_t dtype, void* stream) {
+  return gather_entry("o1d_bwd_input", dy, w, theta_deg, dx, N, C, H, W, K, dtype, Opts(), stream, -1);
+}
+
+o1d_status_t o1d_bwd_weight(const void* x, const void* dy, const float* theta_deg, void* dw, int N, int C, int H,
+                            int W, int K, o1d_dtype_t dtype, void* workspace, size_t workspace_bytes, void* stream) {
+  return bwd_weight_entry("o1d_bwd_weight", x, dy, theta_deg, dw, N, C, H, W, K, dtype, Opts(), workspace,
+                          workspace_bytes, stream);
+}
+
+o1d_status_t o1d_fwd_ex(const void* x, const void* w, const float* theta_deg, void* y, int N, int C, int H, int W,
+                        int K, int stride, o1d_layout_t layout, o1d_sampling_t sampling, o1d_dtype_t dtype,
+                        void* stream) {
+  Opts o;
+  o.stride = stride;
+  o.layout = layout;
+  o.sampling = sampling;
+  return gather_entry("o1d_fwd_ex", x, w, theta_deg, y, N, C, H, W, K, dtype, o, stream, +1);
+}
+
+o1d_status_t o1d_bwd_input_ex(const void* dy, const void* w, const float* theta_deg, void* dx, int N, int C, int H,
+                              int W, int K, int stride, o1d_layout_t layout, o1d_sampling_t sampling,
+                              o1d_dtype_t dtype, void* stream) {
+  Opts o;
+  o.stride = stride;
+  o.layout = layout;
+  o.sampling = sampling;
+  return gather_entry("o1d_bwd_input_ex", dy, w, theta_deg, dx, N, C, H, W, K, dtype, o, stream, -1);
+}
+
+o1d_status_t o1d_bwd_weight_ex(const void* x, const void* dy, const float* theta_deg, void* dw, int N, int C, int H,
+                               int W, int K, int stride, o1d_layout_t layout, o1d_sampling_t sampling,
+                               o1d_dtype_t dtype, void* workspace, size_t workspace_bytes, void* stream) {
+  Opts o;
+  o.stride = stride;
+  o.layout = layout;
+  o.sampling = sampling;
+  return bwd_weight_entry("o1d_bwd_weight_ex", x, dy, theta_deg, dw, N, C, H, W, K, dtype, o, workspace,
+                          workspace_bytes, stream);
+}
+
+o1d_status_t o1d_bwd(const void* x, const void* dy, const void* w, const float* theta_deg, void* dx, void* dw, int N,
+                     int C, int H, int W, int K, o1d_dtype_t dtype, void* workspace, size_t workspace_bytes,
+                     void* stream) {
+  return bwd_entry("o1d_bwd", x, dy, w, theta_deg, dx, dw, N, C, H, W, K, dtype, workspace, workspace_bytes, stream);
+}
+
+const char* o1d_kernel_name(int op, int N, int C, int H, int W, int K, int stride, o1d_layout_t layout,
+                            o1d_sampling_t sampling, o1d_dtype_t dtype, int aligned) {
+  Opts o;
+  o.stride = stride;
+  o.layout = layout;
+  o.sampling = sampling;
+  g_name[0] = '\0';
+  if (op < kOpFwd || op > kOpBwd || (op == kOpBwd && !o.plain())) return g_name;
+  if (check_sizes("o1d_kernel_name", N, C, H, W, K, dtype, o) != O1D_OK || in_elems(N, C, H, W) == 0) return g_name;
+  const Route r = route(op, N, C, H, W, K, dtype, o, aligned != 0);
+  if (r.ok) {
+    name_of(g_name, sizeof(g_name), op, r, dtype, o);
+  } else if (op == kOpBwd) {
+    char a[120], b[120];
+    const Route rd = route(kOpDgrad, N, C, H, W, K, dtype, o, aligned != 0);
+    const Route rw = route(kOpWgrad, N, C, H, W, K, dtype, o, aligned != 0);
+    if (rd.ok && rw.ok) {
+      name_of(a, sizeof(a), kOpDgrad, rd, dtype, o);
+      name_of(b, sizeof(b), kOpWgrad, rw, dtype, o);
+      snprintf(g_name, sizeof(g_name), "%s+%s", a, b);
+    }
+  }
+  return g_name;
+}
+
+const char* o1d_kernel_variant(int i) {
+  // every kernel instantiation compiled into the library, in the names
+  // o1d_kernel_name uses
+  struct Table {
+    char names[128][48];
+    int count = 0;
+    Table() {
+      for (const char* d : {"f32", "bf16"}) {
+        for (int S : o1d::strip::kStrides) {
+          snprintf(names[count++], 48, "strip_gather/%s/S%d/KB32", d, S);
+          snprintf(names[count++], 48, "strip_gather/%s/S%d/KB64", d, S);
+          snprintf(names[count++], 48, "strip_wgrad/%s/S%d/KB32", d, S);
+          snprintf(names[count++], 48, "strip_bwd/%s/S%d/KB32", d, S);
+        }
+        for (const char* l : {"nchw", "nhwc"})
+          for (int rp : {4, 8}) {
+            snprintf(names[count++], 48, "gen_gather/%s/%s/RP%d", d, l, rp);
+            snprintf(names[count++], 48, "gen_wgrad/%s/%s/RP%d", d, l, rp);
+          }
+      }
+    }
+  };
+  static const Table t;  // initialised once, thread-safe
+  return i >= 0 && i < t.count ? t.names[i] : nullptr;
 }
 
 const char* o1d_status_str(o1d_status_t status) {
@@ -232,6 +385,6 @@ const char* o1d_status_str(o1d_status_t status) {
 
 const char* o1d_last_error(void) { return g_last_error; }
 
-const char* o1d_version(void) { return "o1d 0.1.0 (gfx950)"; }
+const char* o1d_version(void) { return "o1d 0.2.0 (gfx950)"; }
 
 }  // extern "C"

@@ -64,4 +64,27 @@ __device__ __forceinline__ bool tap_offset(float theta_deg, int K, int k, int* d
   return true;
 }
 
+// Unrounded offsets of tap k (the rotation of (0, k - pad) by theta, before
+// the floor of Eq. 2): rh = -(k - pad) sin theta, rw = (k - pad) cos theta.
+// Returns false for a non-finite angle (the offsets are then 0).
+__device__ __forceinline__ bool tap_real(float theta_deg, int K, int k, double* rh, double* rw) {
+  if (!isfinite(theta_deg)) {
+    *rh = 0.0;
+    *rw = 0.0;
+    return false;
+  }
+  double s, c;
+  sincos((double)theta_deg * kDegToRad, &s, &c);
+  const double j = (double)(k - (K >> 1));
+  *rh = -j * s;
+  *rw = j * c;
+  return true;
+}
+
+// Fraction of v above floor_snapped(v): zero for a snapped (near-integer) v.
+__device__ __forceinline__ double frac_snapped(double v, int fl) {
+  const double f = v - (double)fl;
+  return fabs(f) <= kSnapEps ? 0.0 : f;
+}
+
 }  // namespace o1d

@@ -1,0 +1,17 @@
+// General kernels (any plane, alignment, stride, layout, discretisation),
+// float32 storage.
+#include "o1d_gen_kernels.h"
+
+namespace o1d {
+
+hipError_t launch_gen_gather_f32(const gen::Plan& pl, int layout, const void* in, const void* w, const float* theta,
+                                void* out, hipStream_t stream) {
+  return gen::gather_t<float>(pl, layout, in, w, theta, out, stream);
+}
+
+hipError_t launch_gen_wgrad_f32(const gen::Plan& pl, int layout, const void* x, const void* dy, const float* theta,
+                               void* dw, float* partial, hipStream_t stream) {
+  return gen::wgrad_t<float>(pl, layout, x, dy, theta, dw, partial, stream);
+}
+
+}  // namespace o1d

@@ -7,7 +7,6 @@
 #pragma once
 
 #include <stddef.h>
-#include <stdlib.h>
 
 #include "o1d_launch.h"
 #include "o1d_plan.h"
@@ -62,8 +61,6 @@ inline int fit_npw(int N, int C, int G, long long slots) {
       npw = n;
     }
   }
-  if (const char* e = getenv("O1D_TUNE_NPW"))
-    if (atoi(e) > 0) npw = cdiv(atoi(e), G) * G;
   return npw;
 }
 
@@ -230,7 +227,7 @@ O1D_STRIP_BDECL(launch_bwd_strip_bf16_k32)
 #undef O1D_STRIP_BDECL
 
 // Fused backward (input and weight gradients in one pass): the weight
-// gradient's plan with mirrored offsets (sign -1), walks of up to 32 cells.
+// gradient's plan with mirrored offsets (sign -1), walks of up to 31 cells.
 inline hipError_t launch_bwd_strip(Dtype dt, const strip::Plan& pl, const void* x, const void* dy, const void* w,
                                    const float* theta, void* dx, void* dw, float* partial, hipStream_t stream) {
   if (pl.KB != 32 || pl.p.sign != -1) return hipErrorInvalidValue;
@@ -238,8 +235,9 @@ inline hipError_t launch_bwd_strip(Dtype dt, const strip::Plan& pl, const void* 
                           : launch_bwd_strip_bf16_k32(pl, x, dy, w, theta, dx, dw, partial, stream);
 }
 
-// Weight gradient: walks of up to 32 cells only (K <= 32; the per-cell
-// accumulators of longer walks do not fit in registers next to the window).
+// Weight gradient: walks of up to 32 cells (the per-cell accumulators of
+// longer walks do not fit in registers next to the window; the general
+// kernels take K > 31).
 inline hipError_t launch_wgrad_strip(Dtype dt, const strip::Plan& pl, const void* x, const void* dy,
                                      const float* theta, void* dw, float* partial, hipStream_t stream) {
   if (pl.KB != 32) return hipErrorInvalidValue;

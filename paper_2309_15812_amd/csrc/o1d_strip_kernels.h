@@ -47,7 +47,6 @@
 #include "o1d_device.h"
 #include "o1d_launch.h"
 #include "o1d_strip.h"
-#include "o1d_strip_asm.h"
 
 namespace o1d {
 namespace strip {
@@ -201,24 +200,28 @@ __device__ __forceinline__ void lds_store(uint32_t a, float v) {
   *(__attribute__((address_space(3))) float*)(uintptr_t)a = v;
 }
 
-// The window step of cell C (generated inline assembly): a run's first
-// cell reloads all R rows, every cell but the walk's last reads the next
-// cell's new row.
+// The window step of cell C: a run's first cell reloads all R rows, every
+// cell but the walk's last reads the next cell's new row (assuming that cell
+// continues the run; a next cell that starts a run reloads every row).  Row
+// i, column k of cell C sits at base + 4 ((C + i) ST + k), so the offsets are
+// immediates; register row (C + i) mod (R + 1) holds row i.  The run bits
+// pass through an empty asm statement so that the test stays a scalar bit
+// test inside the walk instead of being hoisted out of the group loop.
 template <int R, int NC, int ST, int C, int KB>
 __device__ __forceinline__ void window_step(float (&sl)[R + 1][NC], uint32_t& base, uint32_t lb, uint32_t vrb,
                                             uint32_t bits) {
-  constexpr bool kLast = C + 1 == KB;
-  if constexpr (R == kRv && NC == kNv) {
-    if constexpr (kLast)
-      cell_asm_28x1_last<ST, C>(sl, base, lb, vrb, bits);
-    else
-      cell_asm_28x1<ST, C>(sl, base, lb, vrb, bits);
-  } else {
-    static_assert(R == kRd && NC == kNd, "strip shape without a generated window step");
-    if constexpr (kLast)
-      cell_asm_7x4_last<ST, C>(sl, base, lb, vrb, bits);
-    else
-      cell_asm_7x4<ST, C>(sl, base, lb, vrb, bits);
+  uint32_t b = bits;
+  asm volatile("" : "+s"(b));
+  if (b & (1u << (C & 31))) {
+    base = lb + (uint32_t)__builtin_amdgcn_readlane((int)vrb, C);
+#pragma unroll
+    for (int i = 0; i < R; ++i)
+#pragma unroll
+      for (int k = 0; k < NC; ++k) sl[(C + i) % (R + 1)][k] = lds_load(base + 4u * (uint32_t)((C + i) * ST + k));
+  }
+  if constexpr (C + 1 < KB) {
+#pragma unroll
+    for (int k = 0; k < NC; ++k) sl[(C + R) % (R + 1)][k] = lds_load(base + 4u * (uint32_t)((C + R) * ST + k));
   }
 }
 
@@ -568,8 +571,6 @@ __device__ __forceinline__ void gather_groups(const Params& P, const Chan& ch, f
     float sl[R + 1][NC];
     uint32_t base = lb;
     GatherWalk<R, NC, ST, 0, KB>::run(ch.ncells, base, lb, ch.vrb, ch.bits_lo, ch.bits_hi, ch.vw, sl, acc);
-    // the last cell's read-ahead (of a cell that does not exist) may still be in flight
-    asm volatile("s_waitcnt lgkmcnt(0)" ::: "memory");
     __syncthreads();  // every lane has finished reading the tile
     if (task && g < ng) put_block<R, NC, ST, SD>(bk, ch, acc);
     __syncthreads();  // the group's outputs are in the tile
@@ -663,7 +664,6 @@ __device__ __forceinline__ void wgrad_groups(const Params& P, const Chan& ch, fl
     float sl[R + 1][NC];
     uint32_t base = bk.lb;
     WgradWalk<R, NC, ST, 0, KB>::run(ch.ncells, base, bk.lb, ch.vrb, ch.bits_lo, ch.bits_hi, sl, dv, acc);
-    asm volatile("s_waitcnt lgkmcnt(0)" ::: "memory");
     __syncthreads();  // the tile is free
   }
 }
@@ -701,7 +701,7 @@ __device__ __forceinline__ void write_partial(const Params& P, const Prog* pg, f
 // workgroup's images of dy * x[tap k + output] (Eq. 1 differentiated in w),
 // reduced over lanes and waves in a fixed order (no atomics).
 template <typename T, int S, int KB>
-__global__ __launch_bounds__(kThreads) void strip_wgrad(Params P, const T* __restrict__ x, const T* __restrict__ dy,
+__global__ __launch_bounds__(kThreads, 2) void strip_wgrad(Params P, const T* __restrict__ x, const T* __restrict__ dy,
                                                         const float* __restrict__ theta, float* __restrict__ partial) {
   extern __shared__ float smem[];
   Prog* pg = reinterpret_cast<Prog*>(smem);
@@ -791,7 +791,6 @@ __device__ __forceinline__ void bwd_groups(const Params& P, const Chan& ch, floa
     uint32_t base = bk.lb;
     BwdWalk<R, NC, ST, 0, KB - 1, KB>::run(ch.ncells, base, bk.lb, ch.vrb, ch.bits_lo, ch.bits_hi, ch.vw, sl, xv, out,
                                           acc);
-    asm volatile("s_waitcnt lgkmcnt(0)" ::: "memory");
     stg.load(P, xc + next, nn, pre);
     __syncthreads();  // every lane has finished reading the tile
     if (bk.task && bk.g < ng) put_block<R, NC, ST, SD>(bk, ch, out);
@@ -921,6 +920,21 @@ hipError_t resident_per_cu(size_t lds_bytes, int* per_cu) {
   return hipSuccess;
 }
 
+// Raises a kernel's dynamic LDS limit to the whole LDS once per process
+// (the first launch of each instantiation pays for the runtime call).
+template <const void* (*Fn)()>
+hipError_t allow_full_lds() {
+  static std::atomic<int> done{0};
+  if (done.load(std::memory_order_acquire)) return hipSuccess;
+  const hipError_t e = hipFuncSetAttribute(Fn(), hipFuncAttributeMaxDynamicSharedMemorySize, (int)kMaxLdsBytes);
+  if (e == hipSuccess) done.store(1, std::memory_order_release);
+  return e;
+}
+template <typename T, int S, int KB>
+const void* wgrad_fn() { return reinterpret_cast<const void*>(strip_wgrad<T, S, KB>); }
+template <typename T, int S, int KB>
+const void* bwd_fn() { return reinterpret_cast<const void*>(strip_bwd<T, S, KB>); }
+
 template <typename T, int S, int KB>
 hipError_t gather_launch(const Plan& plan, const void* in, const void* w, const float* theta, void* out,
                          hipStream_t stream) {
@@ -938,8 +952,7 @@ hipError_t gather_launch(const Plan& plan, const void* in, const void* w, const 
 template <typename T, int S, int KB>
 hipError_t wgrad_launch(const Plan& pl, const void* x, const void* dy, const float* theta, float* partial,
                         hipStream_t stream) {
-  hipError_t e = hipFuncSetAttribute(reinterpret_cast<const void*>(strip_wgrad<T, S, KB>),
-                                     hipFuncAttributeMaxDynamicSharedMemorySize, (int)kMaxLdsBytes);
+  const hipError_t e = allow_full_lds<wgrad_fn<T, S, KB>>();
   if (e != hipSuccess) return e;
   hipLaunchKernelGGL((strip_wgrad<T, S, KB>), dim3((unsigned)pl.blocks_n, (unsigned)pl.p.C, 1), dim3(kThreads),
                      pl.lds_bytes, stream, pl.p, static_cast<const T*>(x), static_cast<const T*>(dy), theta, partial);
@@ -964,8 +977,7 @@ hipError_t wgrad_t(const Plan& pl, const void* x, const void* dy, const float* t
 template <typename T, int S, int KB>
 hipError_t bwd_launch(const Plan& pl, const void* x, const void* dy, const void* w, const float* theta, void* dx,
                       float* partial, hipStream_t stream) {
-  hipError_t e = hipFuncSetAttribute(reinterpret_cast<const void*>(strip_bwd<T, S, KB>),
-                                     hipFuncAttributeMaxDynamicSharedMemorySize, (int)kMaxLdsBytes);
+  const hipError_t e = allow_full_lds<bwd_fn<T, S, KB>>();
   if (e != hipSuccess) return e;
   hipLaunchKernelGGL((strip_bwd<T, S, KB>), dim3((unsigned)pl.blocks_n, (unsigned)pl.p.C, 1), dim3(kThreads),
                      pl.lds_bytes, stream, pl.p, static_cast<const T*>(x), static_cast<const T*>(dy),

@@ -131,3 +131,33 @@ def test_python_wrapper_refuses_cpu_tensors():
     x = torch.zeros(1, 2, 4, 4)
     with pytest.raises(ValueError):
         ops.fwd(x, torch.zeros(2, 3), torch.zeros(2))
+
+
+def fwd_ex(*, stride=1, layout=0, sampling=0, K=7, N=2, C=3, H=5, W=6, x=P, y=ctypes.c_void_p(0x200000000)):
+    return _lib.call("o1d_fwd_ex", x, Q, R, y, N, C, H, W, K, stride, layout, sampling, F32, None)
+
+
+@pytest.mark.parametrize("kw,status", [
+    (dict(stride=0), INVALID), (dict(stride=-2), INVALID), (dict(layout=2), INVALID), (dict(sampling=3), INVALID),
+    (dict(K=8), INVALID), (dict(x=None), INVALID), (dict(y=P), INVALID),
+    (dict(stride=65), UNSUPPORTED), (dict(K=_lib.MAX_K + 2), UNSUPPORTED),
+])
+def test_ex_entry_points_reject(kw, status):
+    assert fwd_ex(**kw) == status
+    assert _lib.lib().o1d_last_error().decode().startswith("o1d_fwd_ex")
+    a = dict(stride=1, layout=0, sampling=0, K=7)
+    a.update({k: v for k, v in kw.items() if k in a})
+    st = _lib.call("o1d_bwd_input_ex", kw.get("x", P), Q, R, kw.get("y", ctypes.c_void_p(0x200000000)), 2, 3, 5, 6,
+                   a["K"], a["stride"], a["layout"], a["sampling"], F32, None)
+    assert st == status
+
+
+def test_ex_empty_and_workspace():
+    assert fwd_ex(N=0, x=None, y=None) == OK
+    L = _lib.lib()
+    need = L.o1d_bwd_weight_ex_workspace_bytes(2, 3, 40, 40, 15, 2, 1, 1, F32)
+    assert need > 0 and need % (3 * 15 * 4) == 0
+    st = _lib.call("o1d_bwd_weight_ex", P, Q, R, ctypes.c_void_p(0x300000000), 2, 3, 40, 40, 15, 2, 1, 1, F32,
+                   ctypes.c_void_p(0x400000000), need - 4, None)
+    assert st == WORKSPACE
+    assert L.o1d_bwd_weight_ex_workspace_bytes(2, 3, 40, 40, 15, 0, 1, 1, F32) == 0  # invalid stride -> 0
