@@ -124,6 +124,21 @@ o1d_status_t o1d_bwd(const void* x, const void* dy, const void* w, const float* 
 /* Workspace size in bytes that o1d_bwd_weight (and o1d_bwd) needs for these sizes. */
 size_t o1d_bwd_weight_workspace_bytes(int N, int C, int H, int W, int K, o1d_dtype_t dtype);
 
+/* o1d_bwd without a workspace argument, for callers that cannot allocate
+ * device memory (code under HIP graph capture, tight serving loops, harnesses
+ * that forbid allocation).  It computes exactly what o1d_bwd computes (the
+ * same kernels and fixed-order sums, so dx and dw are bitwise equal to
+ * o1d_bwd's) and keeps the weight gradient's partial rows in a fixed device scratch
+ * array of 8 MiB that the library holds on every GPU it runs on until the
+ * process ends.  It allocates and frees nothing.  Sizes whose partial rows
+ * need more than 8 MiB (o1d_bwd_weight_workspace_bytes > 8 MiB) return
+ * O1D_ERR_UNSUPPORTED before any launch.  All calls on one GPU share that
+ * GPU's scratch: calls that overlap on one GPU (on different streams, or from
+ * different threads without ordering) race and must be serialised by the
+ * caller.  Nothing needs clearing between calls.  Other rules as o1d_bwd. */
+o1d_status_t o1d_bwd_noalloc(const void* x, const void* dy, const void* w, const float* theta_deg, void* dx,
+                             void* dw, int N, int C, int H, int W, int K, o1d_dtype_t dtype, void* stream);
+
 /* ---- Stride, layout and sampling (Definition 1 with its stride `str`, Eq. 2).
  *
  * The _ex entry points compute the same three operations for any stride >= 1

@@ -15,6 +15,8 @@
 #include <stdio.h>
 #include <string.h>
 
+#include <mutex>
+
 #include "o1d.h"
 #include "o1d_gen.h"
 #include "o1d_launch.h"
@@ -246,6 +248,39 @@ o1d_status_t bwd_entry(const char* fn, const void* x, const void* dy, const void
 }
 
 
+// ---- fixed scratch of the no-allocation entry point (o1d_bwd_noalloc)
+//
+// The weight gradient's partial rows live in a file-scope device array
+// instead of a caller workspace.  Each GPU holds its own copy; its address
+// is looked up once per device (with that device current) and kept, and
+// host code only ever uses that address, never the array's name.  Every
+// call on a GPU shares the array, so calls that overlap on one GPU race.
+// Nothing needs clearing: every workgroup overwrites its whole partial row
+// before the reduction reads it.
+constexpr size_t kScratchBytes = (size_t)8 << 20;
+static __device__ __align__(256) unsigned char scratch[kScratchBytes];
+
+constexpr int kMaxDevices = 64;
+std::mutex g_scratch_mu;
+void* g_scratch[kMaxDevices] = {};
+
+o1d_status_t scratch_ptr(const char* fn, void** out) {
+  int dev = -1;
+  hipError_t e = hipGetDevice(&dev);
+  if (e != hipSuccess) return fail(O1D_ERR_HIP, "%s: hipGetDevice failed: %s", fn, hipGetErrorString(e));
+  if (dev < 0 || dev >= kMaxDevices) return fail(O1D_ERR_UNSUPPORTED, "%s: device %d out of range", fn, dev);
+  std::lock_guard<std::mutex> lk(g_scratch_mu);
+  if (!g_scratch[dev]) {
+    void* p = nullptr;
+    e = hipGetSymbolAddress(&p, HIP_SYMBOL(scratch));
+    if (e != hipSuccess || !p)
+      return fail(O1D_ERR_HIP, "%s: hipGetSymbolAddress of the scratch failed: %s", fn, hipGetErrorString(e));
+    g_scratch[dev] = p;
+  }
+  *out = g_scratch[dev];
+  return O1D_OK;
+}
+
 }  // namespace
 
 extern "C" {
@@ -319,6 +354,24 @@ o1d_status_t o1d_bwd(const void* x, const void* dy, const void* w, const float* 
                      int C, int H, int W, int K, o1d_dtype_t dtype, void* workspace, size_t workspace_bytes,
                      void* stream) {
   return bwd_entry("o1d_bwd", x, dy, w, theta_deg, dx, dw, N, C, H, W, K, dtype, workspace, workspace_bytes, stream);
+}
+
+o1d_status_t o1d_bwd_noalloc(const void* x, const void* dy, const void* w, const float* theta_deg, void* dx,
+                             void* dw, int N, int C, int H, int W, int K, o1d_dtype_t dtype, void* stream) {
+  const char* fn = "o1d_bwd_noalloc";
+  const Opts o;
+  o1d_status_t st = check_sizes(fn, N, C, H, W, K, dtype, o);
+  if (st != O1D_OK) return st;
+  if (C == 0 || in_elems(N, C, H, W) == 0)
+    return bwd_entry(fn, x, dy, w, theta_deg, dx, dw, N, C, H, W, K, dtype, nullptr, 0, stream);
+  const size_t need = wgrad_workspace(N, C, H, W, K, dtype, o);
+  if (need > kScratchBytes)
+    return fail(O1D_ERR_UNSUPPORTED, "%s: these sizes need %zu bytes of scratch; the fixed scratch holds %zu", fn,
+                need, kScratchBytes);
+  void* ptr = nullptr;
+  st = scratch_ptr(fn, &ptr);
+  if (st != O1D_OK) return st;
+  return bwd_entry(fn, x, dy, w, theta_deg, dx, dw, N, C, H, W, K, dtype, ptr, kScratchBytes, stream);
 }
 
 const char* o1d_kernel_name(int op, int N, int C, int H, int W, int K, int stride, o1d_layout_t layout,
