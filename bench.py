@@ -13,10 +13,14 @@ Infinity Cache, so a step never finds its inputs cached by an earlier step.
 Prints ONE JSON line: value = algorithmic bytes of the step divided by the
 measured time, in GB/s.  The forward reads x and writes y; the backward reads
 x and dy and writes dx (and the C*K weight gradient): 5 tensors of N*C*H*W
-elements.  The "roofline" object reports the dominant
-kernel's algorithmic bytes per launch over its mean duration (HIP events on
-the stream it runs on) against the 8 TB/s HBM peak; "cpu_baseline" times the
-float64 CPU oracle on the same workload.
+elements.  The "roofline" object reports the dominant kernel's algorithmic
+bytes per launch over its mean duration (HIP events on the stream it runs on)
+against the 8 TB/s HBM peak; "cpu_baseline" times the float64 CPU oracle on
+the same workload.  "configs" holds the same per-op figures for the other
+workloads (stage-2 and stage-3 shapes, NHWC, stride 2 on 224^2 planes,
+bilinear sampling), "copy" a plain copy of one headline tensor (the
+achievable-bandwidth reference) and "angle_cost" the time at arbitrary angles
+over the time at theta = 0 for K in {7, 15, 31, 63}.
 """
 from __future__ import annotations
 
@@ -25,6 +29,7 @@ import hashlib
 import json
 import os
 import statistics
+import subprocess
 import sys
 import time
 
@@ -53,6 +58,14 @@ def kernel_source_hash() -> str:
     return h.hexdigest()[:16]
 
 
+def git_sha():
+    try:
+        r = subprocess.run(["git", "-C", ROOT, "rev-parse", "HEAD"], capture_output=True, text=True, timeout=10)
+        return (r.stdout.strip() or None) if r.returncode == 0 else None
+    except (OSError, subprocess.SubprocessError):
+        return None
+
+
 def parse():
     ap = argparse.ArgumentParser(description=__doc__.split("\n\n")[0])
     ap.add_argument("--gpus", type=int, default=1)
@@ -61,52 +74,104 @@ def parse():
     ap.add_argument("--workload", default="metric")
     ap.add_argument("--sets", type=int, default=6, help="rotating buffer sets (cache defeat)")
     ap.add_argument("--no-cpu", action="store_true", help="skip the CPU oracle baseline")
+    ap.add_argument("--no-extra", action="store_true", help="only the headline step (no configs, sweep, copy)")
     ap.add_argument("--cpu-seconds", type=float, default=12.0, help="target CPU work for the oracle sample")
-    ap.add_argument("--angle-sweep", action="store_true", help="time every K of the angle-cost sweep")
     ap.add_argument("--only", default="", help="profiling aid: run only this op (fwd|bwd|bwd_input|bwd_weight), or "
                     "'copy': a plain elementwise copy of one N*C*H*W tensor (reads T bytes, writes T bytes), "
                     "the calibration kernel for the HBM byte counters")
     return ap.parse_args()
 
 
+def out_size(n, s):
+    return (n - 1) // s + 1
+
+
+class Case:
+    """One timed configuration: a workload plus stride, layout and sampling."""
+
+    def __init__(self, wl, stride=1, layout="nchw", sampling="floor", fused=True):
+        self.wl, self.stride, self.layout, self.sampling, self.fused = wl, stride, layout, sampling, fused
+
+    @property
+    def plain(self):
+        return self.stride == 1 and self.layout == "nchw" and self.sampling == "floor"
+
+    def tensor_bytes(self):
+        wl, s = self.wl, self.stride
+        T_in = wl.elems * wl.elem_bytes
+        T_out = wl.N * wl.C * out_size(wl.H, s) * out_size(wl.W, s) * wl.elem_bytes
+        return T_in, T_out, wl.C * wl.K * wl.elem_bytes
+
+    def algorithmic_bytes(self):
+        """Bytes each op must move: read every input once, write every output once."""
+        T_in, T_out, CK = self.tensor_bytes()
+        return {"fwd": T_in + T_out, "bwd": 2 * T_in + T_out + CK, "bwd_input": T_out + T_in,
+                "bwd_weight": T_in + T_out + CK, "copy": 2 * T_in}
+
+    def describe(self):
+        wl = self.wl
+        return (f"{wl.N}x{wl.C}x{wl.H}x{wl.W} K={wl.K} {wl.dtype} {self.layout} stride {self.stride} "
+                f"{self.sampling}, {THETA_TEXT.get(wl.theta, 'theta mode ' + wl.theta)}")
+
+
 class BufferSet:
-    def __init__(self, d, wl, torch, dev, ops):
+    def __init__(self, d, case, torch, dev, ops):
+        wl = case.wl
         dt = torch.float32 if wl.dtype == "f32" else torch.bfloat16
-        self.x = torch.from_numpy(d["x"]).to(dev).to(dt)
-        self.dy = torch.from_numpy(d["dy"]).to(dev).to(dt)
+        P, Q = out_size(wl.H, case.stride), out_size(wl.W, case.stride)
+        x = torch.from_numpy(d["x"]).to(dev).to(dt)
+        dy = torch.from_numpy(d["dy"][:, :, :P, :Q].copy()).to(dev).to(dt)
+        if case.layout == "nhwc":
+            x, dy = x.permute(0, 2, 3, 1).contiguous(), dy.permute(0, 2, 3, 1).contiguous()
+        self.x, self.dy = x, dy
         self.w = torch.from_numpy(d["w"]).to(dev).to(dt)
         self.th = torch.from_numpy(d["theta"]).to(dev)
-        self.y = torch.empty_like(self.x)
+        self.y = torch.empty_like(self.dy)
         self.dx = torch.empty_like(self.x)
         self.dw = torch.empty_like(self.w)
-        need = ops.workspace_bytes(wl.N, wl.C, wl.H, wl.W, wl.K, dt)
+        if case.plain:
+            need = ops.workspace_bytes(wl.N, wl.C, wl.H, wl.W, wl.K, dt)
+        else:
+            need = ops.workspace_bytes_ex(wl.N, wl.C, wl.H, wl.W, wl.K, dt, case.stride, case.layout, case.sampling)
         self.ws = torch.empty(max(need, 1), dtype=torch.uint8, device=dev)
 
 
-def run_ops(ops, b, K, only=""):
-    if only == "copy":
-        # torch's vectorised elementwise kernel: reads x once, writes y once
+def run_op(ops, case, b, name):
+    wl = case.wl
+    if name == "copy":
+        # torch's vectorised elementwise kernel: reads x once, writes one tensor of x's size once
         import torch
-        torch.neg(b.x, out=b.y)
-        return
-    if not only or only == "fwd":
-        ops.fwd(b.x, b.w, b.th, out=b.y)
-    if not only or only == "bwd":
-        ops.bwd(b.x, b.dy, b.w, b.th, out=(b.dx, b.dw), workspace=b.ws)
-    if only == "bwd_input":
-        ops.bwd_input(b.dy, b.w, b.th, out=b.dx)
-    if only == "bwd_weight":
-        ops.bwd_weight(b.x, b.dy, b.th, K, out=b.dw, workspace=b.ws)
+        torch.neg(b.x, out=b.dx)
+    elif case.plain:
+        if name == "fwd":
+            ops.fwd(b.x, b.w, b.th, out=b.y)
+        elif name == "bwd":
+            ops.bwd(b.x, b.dy, b.w, b.th, out=(b.dx, b.dw), workspace=b.ws)
+        elif name == "bwd_input":
+            ops.bwd_input(b.dy, b.w, b.th, out=b.dx)
+        elif name == "bwd_weight":
+            ops.bwd_weight(b.x, b.dy, b.th, wl.K, out=b.dw, workspace=b.ws)
+    else:
+        a = (case.stride, case.layout, case.sampling)
+        if name == "fwd":
+            ops.fwd_ex(b.x, b.w, b.th, *a, out=b.y)
+        elif name == "bwd_input":
+            ops.bwd_input_ex(b.dy, b.w, b.th, (wl.H, wl.W), *a, out=b.dx)
+        elif name == "bwd_weight":
+            ops.bwd_weight_ex(b.x, b.dy, b.th, wl.K, *a, out=b.dw, workspace=b.ws)
+        else:
+            raise ValueError(name)
 
 
-def time_workload(wl, steps, warmup, nsets, torch, ops, synth, only="", per_op=True):
-    """Returns (ms_per_step, {op: [durations ms]})."""
+def time_case(case, names, steps, warmup, nsets, torch, ops, synth):
+    """Returns (ms_per_step, {op: [durations ms]}) for the ops `names` run in turn per step."""
     dev = torch.device("cuda:0")
-    d = synth.make_inputs(wl)
-    sets = [BufferSet(d, wl, torch, dev, ops) for _ in range(nsets)]
+    d = synth.make_inputs(case.wl)
+    sets = [BufferSet(d, case, torch, dev, ops) for _ in range(nsets)]
+    del d
     for i in range(warmup):
-        run_ops(ops, sets[i % nsets], wl.K, only)
-    names = [only] if only else ["fwd", "bwd"]
+        for nm in names:
+            run_op(ops, case, sets[i % nsets], nm)
     stream = torch.cuda.current_stream(dev)
     # One event before every op; the event before a step's first op also ends
     # the previous step's last op, and one more event ends the last step.
@@ -121,25 +186,53 @@ def time_workload(wl, steps, warmup, nsets, torch, ops, synth, only="", per_op=T
     t0 = time.perf_counter()
     for i in range(steps):
         b = sets[i % nsets]
-        if per_op:
-            for nm in names:
-                mark()
-                run_ops(ops, b, wl.K, nm)
-        else:
-            run_ops(ops, b, wl.K, only)
-    if per_op:
-        mark()
+        for nm in names:
+            mark()
+            run_op(ops, case, b, nm)
+    mark()
     torch.cuda.synchronize()
     t1 = time.perf_counter()
     durs = {nm: [] for nm in names}
-    if per_op:
-        for i in range(steps):
-            for j, nm in enumerate(names):
-                k = i * len(names) + j
-                durs[nm].append(ev[k].elapsed_time(ev[k + 1]))
+    for i in range(steps):
+        for j, nm in enumerate(names):
+            k = i * len(names) + j
+            durs[nm].append(ev[k].elapsed_time(ev[k + 1]))
     del sets
     torch.cuda.empty_cache()
     return (t1 - t0) * 1e3 / steps, durs
+
+
+def op_stats(case, durs):
+    ab = case.algorithmic_bytes()
+    out = {}
+    for nm, v in durs.items():
+        mean = statistics.fmean(v)
+        out[nm] = {"ms_mean": round(mean, 5), "ms_median": round(statistics.median(v), 5),
+                   "ms_std": round(statistics.pstdev(v), 5), "bytes": ab[nm],
+                   "GB/s": round(ab[nm] / (mean * 1e-3) / 1e9, 1),
+                   "frac_hbm_peak": round(ab[nm] / (mean * 1e-3) / 1e9 / HBM_PEAK_GBS, 4)}
+    return out
+
+
+def algorithmic_bytes(wl) -> dict:
+    """Bytes each op of the plain (stride 1, NCHW) path must move (T = one N*C*H*W tensor): the forward
+    reads x and writes y; the fused backward reads x and dy and writes dx and dw; the separate gradients
+    read one or two tensors and write one (or dw)."""
+    return Case(wl).algorithmic_bytes()
+
+
+def traffic_for(op_name: str):
+    """HBM bytes per launch from the committed rocprofv3 counter summary, if it
+    was taken on the current kernel sources."""
+    try:
+        with open(TRAFFIC_FILE) as f:
+            rec = json.load(f)
+    except (OSError, ValueError):
+        return None
+    if rec.get("kernel_source_hash") != kernel_source_hash():
+        return None
+    ent = rec.get("ops", {}).get(op_name)
+    return None if ent is None else ent.get("hbm_bytes_per_launch")
 
 
 def cpu_baseline(wl, synth, seconds):
@@ -160,7 +253,7 @@ def cpu_baseline(wl, synth, seconds):
         t_total += time.perf_counter() - t0
         reps += 1
     step_bytes = 5 * wl.elems * wl.elem_bytes + wl.C * wl.K * wl.elem_bytes  # as the GPU step
-    return {
+    out = {
         "value": round(step_bytes * reps / t_total / 1e9, 3),
         "unit": "GB/s",
         "cores": threads,
@@ -170,29 +263,24 @@ def cpu_baseline(wl, synth, seconds):
                   f"{t_total:.1f} s",
         "ms_per_step": round(t_total * 1e3 / reps, 1),
     }
-
-
-def algorithmic_bytes(wl) -> dict:
-    """Bytes each op must move (T = one N*C*H*W tensor): the forward reads x
-    and writes y; the fused backward reads x and dy and writes dx and dw; the
-    separate gradients read one or two tensors and write one (or dw)."""
-    T = wl.elems * wl.elem_bytes
-    CK = wl.C * wl.K * wl.elem_bytes
-    return {"fwd": 2 * T, "bwd": 3 * T + CK, "bwd_input": 2 * T, "bwd_weight": 2 * T + CK, "copy": 2 * T}
-
-
-def traffic_for(op_name: str):
-    """HBM bytes per launch from the committed rocprofv3 counter summary, if it
-    was taken on the current kernel sources."""
-    try:
-        with open(TRAFFIC_FILE) as f:
-            rec = json.load(f)
-    except (OSError, ValueError):
-        return None
-    if rec.get("kernel_source_hash") != kernel_source_hash():
-        return None
-    ent = rec.get("ops", {}).get(op_name)
-    return None if ent is None else ent.get("hbm_bytes_per_launch")
+    # single-threaded oracle on the small forward workload and on a bounded
+    # sample (two images) of the stage-2 workload, scaled per image
+    single = {}
+    for name, planes in (("c1", None), ("c3", 2)):
+        w2 = synth.WORKLOADS[name]
+        d2 = synth.make_inputs(w2, planes=planes)
+        t0 = time.perf_counter()
+        oracle.fwd(d2["x"], d2["w"], d2["theta"], 1)
+        if w2.ops == "fwd+bwd":
+            oracle.bwd_input(d2["dy"], d2["w"], d2["theta"], 1)
+            oracle.bwd_weight(d2["x"], d2["dy"], d2["theta"], w2.K, 1)
+        dt_s = time.perf_counter() - t0
+        n = d2["x"].shape[0]
+        single[name] = {"images": n, "ops": w2.ops, "seconds": round(dt_s, 3),
+                        "ms_per_image": round(dt_s * 1e3 / n, 2),
+                        "ms_full_workload_est": round(dt_s * 1e3 * w2.N / n, 1)}
+    out["single_thread"] = single
+    return out
 
 
 def main():
@@ -208,24 +296,17 @@ def main():
     from paper_2309_15812_amd import ops, synth
 
     wl = synth.WORKLOADS[args.workload]
+    head = Case(wl)
     T = wl.elems * wl.elem_bytes
     print(f"[bench] workload {wl} T={T / 1e6:.2f} MB sets={args.sets}", file=sys.stderr, flush=True)
-    ms, durs = time_workload(wl, args.steps, args.warmup, args.sets, torch, ops, synth, args.only)
+    names = [args.only] if args.only else ["fwd", "bwd"]
+    ms, durs = time_case(head, names, args.steps, args.warmup, args.sets, torch, ops, synth)
     print(f"[bench] {ms:.4f} ms/step", file=sys.stderr, flush=True)
 
-    op_bytes = algorithmic_bytes(wl)
-    per_op = {}
-    for nm, v in durs.items():
-        mean = statistics.fmean(v)
-        per_op[nm] = {
-            "ms_mean": round(mean, 5),
-            "ms_median": round(statistics.median(v), 5),
-            "ms_std": round(statistics.pstdev(v), 5),
-            "GB/s": round(op_bytes[nm] / (mean * 1e-3) / 1e9, 1),
-            "frac_hbm_peak": round(op_bytes[nm] / (mean * 1e-3) / 1e9 / HBM_PEAK_GBS, 4),
-        }
+    per_op = op_stats(head, durs)
     dominant = max(per_op, key=lambda k: per_op[k]["ms_mean"])
     dom_ms = per_op[dominant]["ms_mean"]
+    op_bytes = head.algorithmic_bytes()
     achieved = op_bytes[dominant] / (dom_ms * 1e-3) / 1e9
     step_bytes = sum(op_bytes[k] for k in durs)
     out = {
@@ -262,16 +343,40 @@ def main():
             "ms_per_launch": dom_ms,
         },
         "ops": per_op,
+        "kernel_source_hash": kernel_source_hash(),
+        "git_sha": git_sha(),
     }
 
-    if not args.only:
-        # Angle cost: the same shapes at theta = 0, 90 and uniform continuous angles.
+    if not args.only and not args.no_extra:
+        # the achievable bandwidth: a plain copy of one headline tensor
+        _, dc = time_case(head, ["copy"], 20, 5, args.sets, torch, ops, synth)
+        out["copy"] = op_stats(head, dc)["copy"]
+        print(f"[bench] copy: {out['copy']}", file=sys.stderr, flush=True)
+        # the other workloads, per op
+        W = synth.WORKLOADS
+        cases = {
+            "c2_stage1_fwd": (Case(W["c2"]), ["fwd"]),
+            "c3_stage2": (Case(W["c3"]), ["fwd", "bwd"]),
+            "c4_stage3_bf16": (Case(W["c4"]), ["fwd", "bwd"]),
+            "nhwc_stage1": (Case(W["metric"], layout="nhwc"), ["fwd", "bwd_input", "bwd_weight"]),
+            "nhwc_stage3_bf16": (Case(W["c4"], layout="nhwc"), ["fwd", "bwd_input", "bwd_weight"]),
+            "stride2_224": (Case(W["metric"].replace(name="s2", N=8, H=224, W=224), stride=2),
+                            ["fwd", "bwd_input", "bwd_weight"]),
+            "bilinear_stage1": (Case(W["metric"], sampling="bilinear"), ["fwd", "bwd_input", "bwd_weight"]),
+        }
+        cfg = {}
+        for key, (case, nm) in cases.items():
+            m, dd = time_case(case, nm, 20, 5, 3, torch, ops, synth)
+            cfg[key] = {"workload": case.describe(), "ms_per_step": round(m, 4), "ops": op_stats(case, dd)}
+            print(f"[bench] {key}: {m:.4f} ms/step", file=sys.stderr, flush=True)
+        out["configs"] = cfg
+        # angle cost: the same shapes at theta = 0, 90 and uniform continuous angles
         sweep = {}
-        for K in ([7, 15, 31, 63] if args.angle_sweep else [31]):
-            base = synth.WORKLOADS["c5"].replace(K=K)
+        for K in (7, 15, 31, 63):
+            base = W["c5"].replace(K=K)
             res = {}
             for mode in ("zero", "ninety", "uniform"):
-                m, dd = time_workload(base.replace(theta=mode), 20, 5, 3, torch, ops, synth)
+                m, dd = time_case(Case(base.replace(theta=mode)), ["fwd", "bwd"], 20, 5, 3, torch, ops, synth)
                 res[mode] = {"step_ms": round(m, 4), "fwd_ms": round(statistics.fmean(dd["fwd"]), 4)}
             r_step = max(v["step_ms"] for v in res.values()) / res["zero"]["step_ms"]
             r_fwd = max(v["fwd_ms"] for v in res.values()) / res["zero"]["fwd_ms"]

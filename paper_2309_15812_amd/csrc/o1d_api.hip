@@ -83,9 +83,10 @@ bool vec_aligned(const void* p, o1d_dtype_t dt) { return ((uintptr_t)p % (dt == 
 
 enum OpKind { kOpFwd = 0, kOpDgrad = 1, kOpWgrad = 2, kOpBwd = 3 };
 
-// The kernels one op runs.  For the fused backward (kOpBwd) the route is ok
-// only where the fused strip kernel applies (its plan in `sp`); otherwise
-// o1d_bwd runs the input gradient's route and then the weight gradient's.
+// The kernels one op runs.  For the fused backward (kOpBwd) the route is the
+// one-pass strip kernel, else the one-pass general kernel; where neither
+// applies (the route is not ok) o1d_bwd runs the input gradient's route and
+// then the weight gradient's.
 struct Route {
   bool ok = false;
   bool use_strip = false;
@@ -103,13 +104,16 @@ Route route(int op, int N, int C, int H, int W, int K, o1d_dtype_t dt, const Opt
     }
   }
   if (op == kOpBwd) {
-    if (o.plain()) {
-      r.sp = o1d::strip::plan_strip(N, C, H, W, K, -1, 1, aligned);
-      if (r.sp.ok) r.ok = r.use_strip = true;
+    if (!o.plain()) return r;
+    r.sp = o1d::strip::plan_strip(N, C, H, W, K, -1, 1, aligned);
+    if (r.sp.ok) {
+      r.ok = r.use_strip = true;
+      return r;
     }
-    return r;  // otherwise: not ok, the two separate routes run
+    // the general one-pass kernel; where it does not apply, the two separate routes run
   }
-  const int gop = op == kOpFwd ? o1d::gen::kFwd : (op == kOpDgrad ? o1d::gen::kDgrad : o1d::gen::kWgrad);
+  const int gop = op == kOpFwd ? o1d::gen::kFwd
+                               : (op == kOpDgrad ? o1d::gen::kDgrad : (op == kOpWgrad ? o1d::gen::kWgrad : o1d::gen::kBwd));
   r.gp = o1d::gen::plan_gen(gop, o.layout == O1D_NHWC ? o1d::gen::kNHWC : o1d::gen::kNCHW, N, C, H, W, K, o.stride,
                             o.sampling == O1D_BILINEAR ? 1 : 0, (int)elem_size(dt));
   r.ok = r.gp.ok;
@@ -125,10 +129,11 @@ size_t route_parts(const Route& r) { return r.use_strip ? (size_t)r.sp.blocks_n 
 // (the fused backward's strip plan has the weight gradient's partial count).
 size_t wgrad_workspace(int N, int C, int H, int W, int K, o1d_dtype_t dt, const Opts& o) {
   size_t parts = 0;
-  for (int a = 0; a < 2; ++a) {
-    const Route r = route(kOpWgrad, N, C, H, W, K, dt, o, a != 0);
-    if (r.ok && route_parts(r) > parts) parts = route_parts(r);
-  }
+  for (int a = 0; a < 2; ++a)
+    for (int op : {kOpWgrad, kOpBwd}) {
+      const Route r = route(op, N, C, H, W, K, dt, o, a != 0);
+      if (r.ok && route_parts(r) > parts) parts = route_parts(r);
+    }
   return parts * (size_t)C * (size_t)K * sizeof(float);
 }
 
@@ -207,7 +212,8 @@ void name_of(char* buf, size_t n, int op, const Route& r, o1d_dtype_t dt, const 
   if (r.use_strip)
     snprintf(buf, n, "strip_%s/%s/S%d/KB%d", fam[op], dt_name(dt), r.sp.S, r.sp.KB);
   else
-    snprintf(buf, n, "gen_%s/%s/%s/RP%d", fam[op], dt_name(dt), o.layout == O1D_NHWC ? "nhwc" : "nchw", r.gp.p.RP);
+    snprintf(buf, n, "gen_%s/%s/%s/RP%d%s", fam[op], dt_name(dt), o.layout == O1D_NHWC ? "nhwc" : "nchw", r.gp.p.RP,
+             op >= kOpWgrad ? (r.gp.p.KB == 32 ? "/KB32" : (r.gp.p.KB == 64 ? "/KB64" : "/KB128")) : "");
 }
 
 o1d_status_t bwd_entry(const char* fn, const void* x, const void* dy, const void* w, const float* theta_deg,
@@ -239,9 +245,10 @@ o1d_status_t bwd_entry(const char* fn, const void* x, const void* dy, const void
     return fail(O1D_ERR_INVALID, "%s: workspace overlaps a tensor", fn);
   const bool va = vec_aligned(x, dtype) && vec_aligned(dy, dtype) && vec_aligned(dx, dtype);
   const Route r = route(kOpBwd, N, C, H, W, K, dtype, o, va);
-  if (r.ok)
-    return hip_status(fn, o1d::launch_bwd_strip((o1d::Dtype)dtype, r.sp, x, dy, w, theta_deg, dx, dw,
-                                                static_cast<float*>(workspace), s));
+  float* part = static_cast<float*>(workspace);
+  if (r.ok && r.use_strip)
+    return hip_status(fn, o1d::launch_bwd_strip((o1d::Dtype)dtype, r.sp, x, dy, w, theta_deg, dx, dw, part, s));
+  if (r.ok) return hip_status(fn, o1d::launch_gen_bwd((o1d::Dtype)dtype, r.gp, x, dy, w, theta_deg, dx, dw, part, s));
   st = gather_entry(fn, dy, w, theta_deg, dx, N, C, H, W, K, dtype, o, stream, -1);
   if (st != O1D_OK) return st;
   return wgrad_dispatch(fn, x, dy, theta_deg, dw, N, C, H, W, K, dtype, o, workspace, s);
@@ -403,7 +410,7 @@ const char* o1d_kernel_variant(int i) {
   // every kernel instantiation compiled into the library, in the names
   // o1d_kernel_name uses
   struct Table {
-    char names[128][48];
+    char names[192][48];
     int count = 0;
     Table() {
       for (const char* d : {"f32", "bf16"}) {
@@ -416,7 +423,11 @@ const char* o1d_kernel_variant(int i) {
         for (const char* l : {"nchw", "nhwc"})
           for (int rp : {4, 8}) {
             snprintf(names[count++], 48, "gen_gather/%s/%s/RP%d", d, l, rp);
-            snprintf(names[count++], 48, "gen_wgrad/%s/%s/RP%d", d, l, rp);
+            for (int kb : {32, 64, 128}) {
+              if (rp == 8 && kb != 32) continue;  // eight outputs per lane only with 32 sums
+              snprintf(names[count++], 48, "gen_wgrad/%s/%s/RP%d/KB%d", d, l, rp, kb);
+              if (l[1] == 'c') snprintf(names[count++], 48, "gen_bwd/%s/%s/RP%d/KB%d", d, l, rp, kb);
+            }
           }
       }
     }

@@ -14,4 +14,9 @@ hipError_t launch_gen_wgrad_bf16(const gen::Plan& pl, int layout, const void* x,
   return gen::wgrad_t<uint16_t>(pl, layout, x, dy, theta, dw, partial, stream);
 }
 
+hipError_t launch_gen_bwd_bf16(const gen::Plan& pl, const void* x, const void* dy, const void* w, const float* theta,
+                             void* dx, void* dw, float* partial, hipStream_t stream) {
+  return gen::bwd_t<uint16_t>(pl, x, dy, w, theta, dx, dw, partial, stream);
+}
+
 }  // namespace o1d

@@ -25,7 +25,7 @@ def _candidates():
             for H, W in ((M, M), (max(1, M // 3), M), (M, max(4, (M // 3) // 4 * 4))):
                 out.append((3, 4, H, W, K, _lib.O1D_NCHW, True))
     # general kernels: ragged or unaligned NCHW, NHWC, small and large planes
-    for K in (7, 31, 63):
+    for K in (7, 31, 63, 127):
         for H, W in ((14, 14), (5, 9), (30, 30), (40, 33), (130, 70)):
             out.append((3, 4, H, W, K, _lib.O1D_NCHW, False))
             out.append((3, 4, H, W, K, _lib.O1D_NHWC, True))

@@ -33,11 +33,13 @@ def test_planned_names_are_compiled_variants():
     ((0, 64, 96, 56, 56, 31), "strip_gather/f32/S87/KB32"),
     ((3, 64, 96, 56, 56, 31), "strip_bwd/f32/S87/KB32"),
     ((3, 64, 192, 28, 28, 31), "strip_bwd/f32/S63/KB32"),
-    # K = 63: strip gather, general weight gradient (the fused kernel stops at 31 cells)
+    # K = 63: strip gather; both gradients in the general one-pass kernel (the
+    # strip one stops at 31 cells)
     ((0, 32, 256, 56, 56, 63), "strip_gather/f32/S119/KB64"),
-    ((3, 32, 256, 56, 56, 63), "strip_gather/f32/S119/KB64+gen_wgrad/f32/nchw/RP8"),
+    ((3, 32, 256, 56, 56, 63), "gen_bwd/f32/nchw/RP4/KB64"),
     # 14 x 14 planes (W not a multiple of 4): general kernels, four rows per lane
     ((0, 64, 384, 14, 14, 31), "gen_gather/f32/nchw/RP4"),
+    ((3, 64, 384, 14, 14, 31), "gen_bwd/f32/nchw/RP4/KB32"),
     # planes too large for the strip tiles
     ((0, 1, 2, 224, 224, 31), "gen_gather/f32/nchw/RP8"),
 ])
@@ -55,6 +57,8 @@ def test_routing_of_options():
     assert _lib.kernel_name(0, 2, 4, 56, 56, 30) == ""
     assert _lib.kernel_name(0, 0, 4, 56, 56, 31) == ""
     assert _lib.kernel_name(3, 2, 4, 56, 56, 31, 2) == ""  # o1d_bwd has no stride
+    # unaligned tensors: the general one-pass backward
+    assert _lib.kernel_name(3, 2, 4, 56, 56, 31, aligned=False) == "gen_bwd/f32/nchw/RP8/KB32"
 
 
 def test_workspace_sizes_cover_every_route():
