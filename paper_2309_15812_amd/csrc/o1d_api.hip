@@ -8,6 +8,10 @@
 //    W a multiple of 4, vector-aligned tensors, planes whose zero-margined
 //    tile fits the compiled tile strides; gathers for K <= 63, the weight
 //    gradient and the fused backward for K <= 31;
+//  * plane kernels (o1d_plane*.h): NCHW planes small enough that a whole
+//    plane, for a group of images, fits in LDS (lanes over images; any
+//    stride, both discretisations, the fused backward at stride 1 rounding
+//    down);
 //  * general kernels (o1d_gen*.h): everything else the ABI accepts.
 #include <hip/hip_runtime.h>
 #include <stdarg.h>
@@ -20,6 +24,7 @@
 #include "o1d.h"
 #include "o1d_gen.h"
 #include "o1d_launch.h"
+#include "o1d_plane.h"
 #include "o1d_strip.h"
 
 namespace {
@@ -83,45 +88,63 @@ bool vec_aligned(const void* p, o1d_dtype_t dt) { return ((uintptr_t)p % (dt == 
 
 enum OpKind { kOpFwd = 0, kOpDgrad = 1, kOpWgrad = 2, kOpBwd = 3 };
 
-// The kernels one op runs.  For the fused backward (kOpBwd) the route is the
-// one-pass strip kernel, else the one-pass general kernel; where neither
-// applies (the route is not ok) o1d_bwd runs the input gradient's route and
-// then the weight gradient's.
+// The kernels one op runs: the strip kernels where they apply, else the
+// plane kernels, else the general kernels.  For the fused backward (kOpBwd)
+// the route is a one-pass kernel of the same order; where none applies (the
+// route is not ok) o1d_bwd runs the input gradient's route and then the
+// weight gradient's.
+enum class Family { None, Strip, Plane, Gen };
+
 struct Route {
   bool ok = false;
-  bool use_strip = false;
+  Family fam = Family::None;
   o1d::strip::Plan sp;
+  o1d::plane::Plan pp;
   o1d::gen::Plan gp;
 };
 
 Route route(int op, int N, int C, int H, int W, int K, o1d_dtype_t dt, const Opts& o, bool aligned) {
   Route r;
-  if (o.plain() && op != kOpBwd) {
-    r.sp = o1d::strip::plan_strip(N, C, H, W, K, op == kOpDgrad ? -1 : 1, op == kOpWgrad ? 1 : 0, aligned);
+  if (op == kOpBwd && !o.plain()) return r;
+  if (o.plain()) {
+    // the fused backward has the weight gradient's strip plan
+    r.sp = o1d::strip::plan_strip(N, C, H, W, K, op == kOpDgrad || op == kOpBwd ? -1 : 1,
+                                  op == kOpWgrad || op == kOpBwd ? 1 : 0, aligned);
     if (r.sp.ok) {
-      r.ok = r.use_strip = true;
+      r.ok = true;
+      r.fam = Family::Strip;
       return r;
     }
   }
-  if (op == kOpBwd) {
-    if (!o.plain()) return r;
-    r.sp = o1d::strip::plan_strip(N, C, H, W, K, -1, 1, aligned);
-    if (r.sp.ok) {
-      r.ok = r.use_strip = true;
+  const int sampling = o.sampling == O1D_BILINEAR ? 1 : 0;
+  if (o.layout == O1D_NCHW) {
+    r.pp = o1d::plane::plan_plane(op, N, C, H, W, K, o.stride, sampling, (int)elem_size(dt), aligned);
+    if (r.pp.ok) {
+      r.ok = true;
+      r.fam = Family::Plane;
       return r;
     }
-    // the general one-pass kernel; where it does not apply, the two separate routes run
   }
   const int gop = op == kOpFwd ? o1d::gen::kFwd
                                : (op == kOpDgrad ? o1d::gen::kDgrad : (op == kOpWgrad ? o1d::gen::kWgrad : o1d::gen::kBwd));
   r.gp = o1d::gen::plan_gen(gop, o.layout == O1D_NHWC ? o1d::gen::kNHWC : o1d::gen::kNCHW, N, C, H, W, K, o.stride,
-                            o.sampling == O1D_BILINEAR ? 1 : 0, (int)elem_size(dt));
-  r.ok = r.gp.ok;
+                            sampling, (int)elem_size(dt));
+  if (r.gp.ok) {
+    r.ok = true;
+    r.fam = Family::Gen;
+  }
   return r;
 }
 
 // Partial rows per channel of the weight gradient's route.
-size_t route_parts(const Route& r) { return r.use_strip ? (size_t)r.sp.blocks_n : r.gp.parts; }
+size_t route_parts(const Route& r) {
+  switch (r.fam) {
+    case Family::Strip: return (size_t)r.sp.blocks_n;
+    case Family::Plane: return r.pp.parts;
+    case Family::Gen: return r.gp.parts;
+    default: return 0;
+  }
+}
 
 // The weight gradient's workspace holds one partial row of K float32 per
 // channel and workgroup.  Its size must not depend on pointer alignment, so
@@ -169,7 +192,10 @@ o1d_status_t gather_entry(const char* fn, const void* in, const void* w, const f
   const bool va = vec_aligned(in, dt) && vec_aligned(out, dt);
   const Route r = route(sign > 0 ? kOpFwd : kOpDgrad, N, C, H, W, K, dt, o, va);
   if (!r.ok) return unsupported(fn, N, C, H, W, K);
-  if (r.use_strip) return hip_status(fn, o1d::launch_gather_strip((o1d::Dtype)dt, r.sp, in, w, theta, out, s));
+  if (r.fam == Family::Strip)
+    return hip_status(fn, o1d::launch_gather_strip((o1d::Dtype)dt, r.sp, in, w, theta, out, s));
+  if (r.fam == Family::Plane)
+    return hip_status(fn, o1d::launch_plane_gather((o1d::Dtype)dt, r.pp, in, w, theta, out, s));
   return hip_status(fn, o1d::launch_gen_gather((o1d::Dtype)dt, r.gp, (int)o.layout, in, w, theta, out, s));
 }
 
@@ -180,7 +206,10 @@ o1d_status_t wgrad_dispatch(const char* fn, const void* x, const void* dy, const
   const Route r = route(kOpWgrad, N, C, H, W, K, dt, o, va);
   if (!r.ok) return unsupported(fn, N, C, H, W, K);
   float* part = static_cast<float*>(workspace);
-  if (r.use_strip) return hip_status(fn, o1d::launch_wgrad_strip((o1d::Dtype)dt, r.sp, x, dy, theta, dw, part, s));
+  if (r.fam == Family::Strip)
+    return hip_status(fn, o1d::launch_wgrad_strip((o1d::Dtype)dt, r.sp, x, dy, theta, dw, part, s));
+  if (r.fam == Family::Plane)
+    return hip_status(fn, o1d::launch_plane_wgrad((o1d::Dtype)dt, r.pp, x, dy, theta, dw, part, s));
   return hip_status(fn, o1d::launch_gen_wgrad((o1d::Dtype)dt, r.gp, (int)o.layout, x, dy, theta, dw, part, s));
 }
 
@@ -209,8 +238,11 @@ o1d_status_t bwd_weight_entry(const char* fn, const void* x, const void* dy, con
 
 void name_of(char* buf, size_t n, int op, const Route& r, o1d_dtype_t dt, const Opts& o) {
   static const char* fam[] = {"gather", "gather", "wgrad", "bwd"};
-  if (r.use_strip)
+  if (r.fam == Family::Strip)
     snprintf(buf, n, "strip_%s/%s/S%d/KB%d", fam[op], dt_name(dt), r.sp.S, r.sp.KB);
+  else if (r.fam == Family::Plane)
+    snprintf(buf, n, "plane_%s/%s/RP%d%s", fam[op], dt_name(dt), r.pp.p.RP,
+             op >= kOpWgrad ? (r.pp.p.KB == 32 ? "/KB32" : (r.pp.p.KB == 64 ? "/KB64" : "/KB128")) : "");
   else
     snprintf(buf, n, "gen_%s/%s/%s/RP%d%s", fam[op], dt_name(dt), o.layout == O1D_NHWC ? "nhwc" : "nchw", r.gp.p.RP,
              op >= kOpWgrad ? (r.gp.p.KB == 32 ? "/KB32" : (r.gp.p.KB == 64 ? "/KB64" : "/KB128")) : "");
@@ -246,9 +278,12 @@ o1d_status_t bwd_entry(const char* fn, const void* x, const void* dy, const void
   const bool va = vec_aligned(x, dtype) && vec_aligned(dy, dtype) && vec_aligned(dx, dtype);
   const Route r = route(kOpBwd, N, C, H, W, K, dtype, o, va);
   float* part = static_cast<float*>(workspace);
-  if (r.ok && r.use_strip)
+  if (r.fam == Family::Strip)
     return hip_status(fn, o1d::launch_bwd_strip((o1d::Dtype)dtype, r.sp, x, dy, w, theta_deg, dx, dw, part, s));
-  if (r.ok) return hip_status(fn, o1d::launch_gen_bwd((o1d::Dtype)dtype, r.gp, x, dy, w, theta_deg, dx, dw, part, s));
+  if (r.fam == Family::Plane)
+    return hip_status(fn, o1d::launch_plane_bwd((o1d::Dtype)dtype, r.pp, x, dy, w, theta_deg, dx, dw, part, s));
+  if (r.fam == Family::Gen)
+    return hip_status(fn, o1d::launch_gen_bwd((o1d::Dtype)dtype, r.gp, x, dy, w, theta_deg, dx, dw, part, s));
   st = gather_entry(fn, dy, w, theta_deg, dx, N, C, H, W, K, dtype, o, stream, -1);
   if (st != O1D_OK) return st;
   return wgrad_dispatch(fn, x, dy, theta_deg, dw, N, C, H, W, K, dtype, o, workspace, s);
@@ -429,6 +464,13 @@ const char* o1d_kernel_variant(int i) {
               if (l[1] == 'c') snprintf(names[count++], 48, "gen_bwd/%s/%s/RP%d/KB%d", d, l, rp, kb);
             }
           }
+        for (int rp : {2, 4}) {
+          snprintf(names[count++], 48, "plane_gather/%s/RP%d", d, rp);
+          for (int kb : {32, 64, 128}) {
+            snprintf(names[count++], 48, "plane_wgrad/%s/RP%d/KB%d", d, rp, kb);
+            snprintf(names[count++], 48, "plane_bwd/%s/RP%d/KB%d", d, rp, kb);
+          }
+        }
       }
     }
   };

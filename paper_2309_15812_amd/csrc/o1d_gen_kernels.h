@@ -29,23 +29,13 @@
 
 #include "o1d_device.h"
 #include "o1d_gen.h"
-
-#include <utility>
+#include "o1d_wave.h"
 
 namespace o1d {
 namespace gen {
 namespace {
 
-// Calls f(integral_constant<int, I>) for I = 0 .. N - 1, unrolled whatever
-// the loop body's size (the per-cell sums must stay compile-time indexed).
-template <class F, int... I>
-__device__ __forceinline__ void static_for_impl(F&& f, std::integer_sequence<int, I...>) {
-  (f(std::integral_constant<int, I>{}), ...);
-}
-template <int N, class F>
-__device__ __forceinline__ void static_for(F&& f) {
-  static_for_impl(f, std::make_integer_sequence<int, N>{});
-}
+using wave::static_for;
 
 // Per-channel cell table in LDS (ncap cells per channel):
 //   cw[2 j], cw[2 j + 1]: tile offset a TC + b (mirrored for the input
@@ -427,37 +417,6 @@ __global__ __launch_bounds__(kThreads) void gen_gather(Params P, const T* __rest
 
 // ---------------------------------------------------------------- weight gradients
 
-// Sum over the 64 lanes of each of the 32 values acc[O .. O + 31]: five
-// halving exchanges leave lane L with the sum over its lane pair of value
-// O + ((L >> 1) & 31); the last exchange adds the pair.  Returns the total of
-// that value.  acc[O .. O + 31] is consumed.
-template <int O, int KB>
-__device__ __forceinline__ float wave_sum32(float (&acc)[KB]) {
-  const int lane = threadIdx.x & 63;
-#pragma unroll
-  for (int m = 32, half = 16; m >= 2; m >>= 1, half >>= 1) {
-    // select with bit masks on the loaded values, so that no select of two
-    // array addresses (a run-time index, which would put acc in scratch) appears
-    const int up = (lane & m) ? -1 : 0;
-#pragma unroll
-    for (int i = 0; i < half; ++i) {
-      const int lo = __float_as_int(acc[O + i]), hi = __float_as_int(acc[O + i + half]);
-      const float give = __int_as_float((lo & up) | (hi & ~up));
-      const float keep = __int_as_float((hi & up) | (lo & ~up));
-      acc[O + i] = keep + __shfl_xor(give, m, 64);
-    }
-  }
-  return acc[O] + __shfl_xor(acc[O], 1, 64);
-}
-
-template <int KB, int H>
-__device__ __forceinline__ void wave_sums(float (&acc)[KB], float* red) {
-  const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6;
-  const float s = wave_sum32<32 * H>(acc);
-  if ((lane & 1) == 0) red[wave * KB + 32 * H + ((lane >> 1) & 31)] = s;
-  if constexpr (32 * (H + 1) < KB) wave_sums<KB, H + 1>(acc, red);
-}
-
 // Adds the workgroup's sums of cells j0 .. j0 + KB - 1 of channel ch, times
 // the cells' coefficients, to the per-tap sums dwacc[ch * K + tap] in a fixed
 // order.  Every lane holds sums of channel ch (zero where it had no task).
@@ -465,7 +424,7 @@ __device__ __forceinline__ void wave_sums(float (&acc)[KB], float* red) {
 template <int KB>
 __device__ __forceinline__ void fold_cells(const Params& P, const Cells& cl, float (&acc)[KB], int ch, int j0,
                                            float* red, float* dwacc) {
-  wave_sums<KB, 0>(acc, red);
+  wave::sums<KB>(acc, red);
   __syncthreads();
   if (threadIdx.x == 0) {
     const int nc = cl.cnt[ch];

@@ -14,7 +14,30 @@ __global__ __launch_bounds__(kThreads) void fill_zero(T* __restrict__ dst, size_
   if (i < count) dst[i] = from_f32<T>(0.f);
 }
 
+// dw[i] = sum over j < parts of partial[j CK + i], in a fixed order.
+template <typename T>
+__global__ __launch_bounds__(kThreads) void partial_sum(const float* __restrict__ partial, T* __restrict__ dw, int CK,
+                                                        int parts) {
+  const int i = blockIdx.x * blockDim.x + threadIdx.x;
+  if (i >= CK) return;
+  float s = 0.f;
+  for (int j = 0; j < parts; ++j) s += partial[(size_t)j * CK + i];
+  dw[i] = from_f32<T>(s);
+}
+
 }  // namespace
+
+hipError_t launch_partial_sum(Dtype dt, const float* partial, void* dw, int CK, int parts, hipStream_t stream) {
+  if (CK <= 0) return hipSuccess;
+  const unsigned blocks = (unsigned)((CK + kThreads - 1) / kThreads);
+  if (dt == Dtype::F32)
+    hipLaunchKernelGGL(partial_sum<float>, dim3(blocks), dim3(kThreads), 0, stream, partial, static_cast<float*>(dw),
+                       CK, parts);
+  else
+    hipLaunchKernelGGL(partial_sum<uint16_t>, dim3(blocks), dim3(kThreads), 0, stream, partial,
+                       static_cast<uint16_t*>(dw), CK, parts);
+  return hipGetLastError();
+}
 
 hipError_t launch_zero(Dtype dt, void* dst, size_t count, hipStream_t stream) {
   if (count == 0) return hipSuccess;

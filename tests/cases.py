@@ -24,6 +24,11 @@ def _candidates():
         for M in range(4, 132, 4):
             for H, W in ((M, M), (max(1, M // 3), M), (M, max(4, (M // 3) // 4 * 4))):
                 out.append((3, 4, H, W, K, _lib.O1D_NCHW, True))
+    # plane kernels: small NCHW planes with at least eight images
+    for K in (7, 31, 63, 127):
+        for H, W in ((14, 14), (16, 16), (5, 9), (13, 20)):
+            out.append((8, 4, H, W, K, _lib.O1D_NCHW, True))
+            out.append((8, 4, H, W, K, _lib.O1D_NCHW, False))
     # general kernels: ragged or unaligned NCHW, NHWC, small and large planes
     for K in (7, 31, 63, 127):
         for H, W in ((14, 14), (5, 9), (30, 30), (40, 33), (130, 70)):

@@ -146,7 +146,24 @@ EX = [
 ]
 
 
-@pytest.mark.parametrize("case", EX, ids=lambda c: "-".join(map(str, c)))
+# small planes with at least eight images (the plane kernels): strides,
+# bilinear sampling, image counts that leave a ragged last group of images,
+# planes whose size allows vector accesses of four, two or one element
+PLANE_EX = [
+    (16, 6, 14, 14, 31, "f32", "uniform", 1, "nchw", "floor"),
+    (9, 5, 14, 14, 31, "bf16", "uniform", 1, "nchw", "floor"),
+    (70, 2, 14, 14, 31, "bf16", "discrete8", 1, "nchw", "floor"),
+    (12, 4, 23, 29, 7, "f32", "uniform", 2, "nchw", "floor"),
+    (10, 3, 17, 20, 9, "bf16", "uniform", 3, "nchw", "bilinear"),
+    (16, 4, 14, 14, 31, "f32", "discrete8", 2, "nchw", "bilinear"),
+    (20, 3, 13, 11, 15, "f32", "uniform", 4, "nchw", "floor"),
+    (8, 2, 6, 20, 63, "bf16", "uniform", 1, "nchw", "bilinear"),
+    (40, 3, 7, 7, 31, "f32", "uniform", 1, "nchw", "bilinear"),
+    (33, 3, 10, 6, 15, "f32", "uniform", 1, "nchw", "floor"),
+]
+
+
+@pytest.mark.parametrize("case", EX + PLANE_EX, ids=lambda c: "-".join(map(str, c)))
 def test_stride_layout_sampling(case):
     N, C, H, W, K, dtype, theta, s, layout, sampling = case
     run_ex(N, C, H, W, K, dtype, theta, s, layout, sampling, label=str(case))
