@@ -468,7 +468,7 @@ const char* o1d_kernel_variant(int i) {
           snprintf(names[count++], 48, "plane_gather/%s/RP%d", d, rp);
           for (int kb : {32, 64, 128}) {
             snprintf(names[count++], 48, "plane_wgrad/%s/RP%d/KB%d", d, rp, kb);
-            snprintf(names[count++], 48, "plane_bwd/%s/RP%d/KB%d", d, rp, kb);
+            if (rp == 2 || kb != 128) snprintf(names[count++], 48, "plane_bwd/%s/RP%d/KB%d", d, rp, kb);
           }
         }
       }

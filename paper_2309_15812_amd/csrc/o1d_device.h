@@ -19,14 +19,12 @@ __device__ __forceinline__ T from_f32(float v);
 template <>
 __device__ __forceinline__ float from_f32<float>(float v) { return v; }
 
-// float32 -> bfloat16, IEEE round to nearest, ties to even.  NaN stays a
-// (quiet) NaN; overflow rounds to infinity through the exponent carry.
+// float32 -> bfloat16, IEEE round to nearest, ties to even (gfx950 converts
+// in hardware: v_cvt_pk_bf16_f32).  NaN stays a quiet NaN; overflow rounds
+// to infinity.
 template <>
 __device__ __forceinline__ uint16_t from_f32<uint16_t>(float v) {
-  uint32_t u = __float_as_uint(v);
-  if ((u & 0x7fffffffu) > 0x7f800000u) return (uint16_t)((u >> 16) | 0x0040u);
-  u += 0x7fffu + ((u >> 16) & 1u);
-  return (uint16_t)(u >> 16);
+  return __builtin_bit_cast(uint16_t, (__bf16)v);
 }
 
 // ---------------------------------------------------------------- offsets

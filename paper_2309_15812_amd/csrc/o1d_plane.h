@@ -4,12 +4,13 @@
 // group of images, fits in LDS.  NCHW only; any stride, both discretisations
 // of Eq. (2), K <= 127.
 //
-// A workgroup owns one channel and NI images.  A wave's 64 lanes are NI
-// images times R = 64 / NI neighbouring output columns, and each lane
-// computes RP outputs down its column, so every lane of a wave applies the
-// same cells (tap offsets) at the same time.  The plane is staged in LDS as
-// [row][column][image] (one 32-bit word per image, so a wave's reads of one
-// cell touch NI consecutive words), with a margin of only (RP - 1) rows and
+// A workgroup owns one channel and NI images.  A wave's 64 lanes are NI / 2
+// image pairs times R = 128 / NI neighbouring output columns, and each lane
+// computes RP outputs down its column for its two images, so every lane of a
+// wave applies the same cells (tap offsets) at the same time.  The plane is
+// staged in LDS as [row][column][image] (one 32-bit word per image: a lane
+// reads its pair with one 64-bit access, and a wave's reads of one cell touch
+// consecutive words), with a margin of only (RP - 1) rows and
 // (R - 1) columns (times the stride, plus one for bilinear corners): cells
 // that fall outside the plane for a whole group of RP x R outputs are not
 // visited at all, instead of reading zeros from a margin of K / 2.
@@ -17,13 +18,15 @@
 
 #include <stddef.h>
 
+#include <algorithm>
+
 #include "o1d_launch.h"
 #include "o1d_plan.h"
 
 namespace o1d {
 namespace plane {
 
-constexpr int kThreads = 256;
+constexpr int kThreads = 512;  // eight waves: twice the waves per SIMD of four at the same LDS
 constexpr int kWaves = kThreads / 64;
 constexpr int kMaxK = 127;
 constexpr size_t kLdsBudget = 80 * 1024;  // at least two workgroups per CU
@@ -39,7 +42,7 @@ struct Params {
   int OH, OW;       // this op's output plane (forward, weight gradient: P x Q; input gradient: H x W)
   int SH, SW, dil;  // staged plane (x, or dy for the input gradients) and its lattice step in the H x W frame
   int sig;          // frame rows (columns) per output row (column): forward and weight gradient str, else 1
-  int NI, lni, R;   // lanes: NI images (a power of two, lni its log2) x R output columns
+  int NI, lni, R;   // lanes: NI / 2 image pairs (NI a power of two, lni its log2) x R output columns
   int RP;           // output rows per lane
   int mr, mc;       // tile margins (rows, columns)
   int TRm, TCm;     // tile rows and columns: H + 2 mr, W + 2 mc
@@ -49,16 +52,20 @@ struct Params {
   int ncells;       // cell slots per channel in use at most (K, or 4 K bilinear)
   int ncap;         // table slots (room for reads past the last cell)
   int KB, nck;      // weight gradients: per-cell sums per lane, and groups of KB cells
-  int vt, va;       // elements per global access: staged plane; output-shaped planes (1, 2 or 4)
-  int nchunk;       // image groups = ceil(N / NI)
-  int nblocks;      // C nchunk
-  int cell_off, ival_off, tile_off, aux_off, red_off;  // LDS byte offsets
+  int vt, va;       // elements per global access: staged plane (dividing its width); output-shaped planes
+  int nslot;        // cell tables in LDS
+  int table_bytes;  // bytes per cell table (cells, then their runs at ival_off)
+  int nchunk;       // image groups = ceil(N / NI); work items = C nchunk (channel, image group)
+  int per;          // items per workgroup
+  int nblocks;      // workgroups = ceil(C nchunk / per)
+  int ival_off;                       // byte offset of the cell runs in a table
+  int tile_off, aux_off, red_off;     // LDS byte offsets (tables start at 0)
 };
 
 struct Plan {
   Params p{};
   size_t lds_bytes = 0;
-  size_t parts = 0;  // weight gradient: partial rows per channel (= nchunk)
+  size_t parts = 0;  // weight gradients: partial rows per channel (= nchunk)
   bool ok = false;
 };
 
@@ -86,21 +93,26 @@ inline Plan plan_plane(int op, int N, int C, int H, int W, int K, int str, int m
   q.KB = q.ncells <= 32 ? 32 : (q.ncells <= 64 ? 64 : 128);
   q.nck = cdiv(q.ncells, q.KB);
   const bool reduce = op == kWgrad || op == kBwd;
+  // vector accesses of 4, 2 or 1 elements: a staged chunk stays within one
+  // row; output-shaped planes are copied as flat runs
   auto vec_of = [&](long long e) {
     for (int v = aligned ? 4 : 1; v > 1; v /= 2)
       if (e % v == 0) return v;
     return 1;
   };
-  q.vt = vec_of((long long)q.SH * q.SW);
+  q.vt = vec_of(q.SW);
   q.va = vec_of((long long)q.OH * q.OW);
   double best_score = 0.0;
   for (int NI = 64; NI >= 8; NI /= 2) {
     for (int RP : {4, 2}) {
+      // the fused backward keeps 128 per-cell sums per lane only with two rows
+      // (registers)
+      if (op == kBwd && q.KB == 128 && RP == 4) continue;
       Params p = q;
       p.NI = NI;
       p.lni = 0;
       while ((1 << p.lni) < NI) ++p.lni;
-      p.R = 64 / NI;
+      p.R = 128 / NI;
       p.RP = RP;
       p.mr = (RP - 1) * p.sig + mode;
       p.mc = (p.R - 1) * p.sig + mode;
@@ -116,28 +128,34 @@ inline Plan plan_plane(int op, int N, int C, int H, int W, int K, int str, int m
         p.OSz = (oe + 1) & ~1;
         if ((p.OSz / 2) % 2 == 0) p.OSz += 2;
       }
-      size_t off = 0;
-      p.cell_off = (int)off;
-      off = align16(off + (size_t)p.ncap * 24 + (size_t)(K + 1) * 4);  // cells (offset and weight, row and
-      // column, tap, coefficient), first cell per tap
-      p.ival_off = (int)off;
-      off = align16(off + (size_t)(p.nrg + p.ncg) * 8 + 16);  // cell intervals, cell count
-      p.tile_off = (int)off;
-      off = align16(off + (size_t)p.TRm * p.TCm * NI * 4);
-      p.aux_off = (int)off;
-      off = align16(off + (size_t)NI * p.OSz * esize);
-      p.red_off = (int)off;
-      if (reduce) off = align16(off + (size_t)(kWaves * p.KB + K) * 4);
-      if (off > kLdsBudget) continue;
+      // LDS: nslot cell tables, the tile, the output-shaped tile, the weight
+      // gradients' reduction area
+      p.ival_off = (int)align16((size_t)p.ncap * 24 + (size_t)(2 * K + 1) * 4);  // cells (offset and weight,
+      // row and column, tap, coefficient), first cell per tap, per-tap counts
+      p.table_bytes = (int)align16((size_t)p.ival_off + (size_t)(p.nrg + p.ncg) * 8);  // then the runs
+      size_t rest = align16((size_t)p.TRm * p.TCm * NI * 4) + align16((size_t)NI * p.OSz * esize);
+      if (reduce) rest += align16((size_t)(kWaves * p.KB + K) * 4);
       p.nchunk = cdiv(N, NI);
-      const long long blocks = (long long)C * p.nchunk;
-      if (blocks > 0x7fffffffll) continue;
+      const long long nitem = (long long)C * p.nchunk;
+      if (nitem > 0x7fffffffll) continue;
+      // one work item per workgroup, one cell table
+      p.per = 1;
+      p.nslot = 1;
+      const size_t off = (size_t)p.table_bytes + rest;
+      if (off > kLdsBudget) continue;
+      p.tile_off = p.nslot * p.table_bytes;
+      p.aux_off = p.tile_off + (int)align16((size_t)p.TRm * p.TCm * NI * 4);
+      p.red_off = p.aux_off + (int)align16((size_t)NI * p.OSz * esize);
+      const long long blocks = (nitem + p.per - 1) / p.per;
       p.nblocks = (int)blocks;
       // idle lanes (images past N, rows and columns past the plane), one
-      // table read per cell and RP tile reads, too few workgroups for 256 CUs
+      // table read per cell and RP tile reads, the cells a group's run adds
+      // for its extent (R - 1 columns, RP - 1 rows), too few workgroups for
+      // 256 CUs, a single workgroup per CU
       double score = (double)p.nchunk * NI / N * ((double)p.nrg * RP / p.OH) * ((double)p.ncg * p.R / p.OW) *
-                     (1.0 + 0.5 / RP);
+                     (1.0 + 0.5 / RP) * (1.0 + (double)(p.R - 1) / p.OW) * (1.0 + (double)(RP - 1) / p.OH);
       if (blocks < 640) score *= 640.0 / (double)blocks;
+      if (kMaxLdsBytes / off < 2) score *= 1.5;
       if (!best.ok || score < best_score - 1e-9) {
         best_score = score;
         best.p = p;

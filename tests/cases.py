@@ -26,7 +26,7 @@ def _candidates():
                 out.append((3, 4, H, W, K, _lib.O1D_NCHW, True))
     # plane kernels: small NCHW planes with at least eight images
     for K in (7, 31, 63, 127):
-        for H, W in ((14, 14), (16, 16), (5, 9), (13, 20)):
+        for H, W in ((14, 14), (16, 16), (5, 9), (13, 20), (40, 12), (40, 8)):
             out.append((8, 4, H, W, K, _lib.O1D_NCHW, True))
             out.append((8, 4, H, W, K, _lib.O1D_NCHW, False))
     # general kernels: ragged or unaligned NCHW, NHWC, small and large planes

@@ -37,9 +37,13 @@ def test_planned_names_are_compiled_variants():
     # strip one stops at 31 cells)
     ((0, 32, 256, 56, 56, 63), "strip_gather/f32/S119/KB64"),
     ((3, 32, 256, 56, 56, 63), "gen_bwd/f32/nchw/RP4/KB64"),
-    # 14 x 14 planes (W not a multiple of 4): general kernels, four rows per lane
-    ((0, 64, 384, 14, 14, 31), "gen_gather/f32/nchw/RP4"),
-    ((3, 64, 384, 14, 14, 31), "gen_bwd/f32/nchw/RP4/KB32"),
+    # 14 x 14 planes (W not a multiple of 4) with many images: plane kernels
+    # (lanes over images), two rows per lane
+    ((0, 64, 384, 14, 14, 31), "plane_gather/f32/RP2"),
+    ((3, 64, 384, 14, 14, 31), "plane_bwd/f32/RP2/KB32"),
+    ((0, 64, 384, 14, 14, 31, 1, 0, 0, 1), "plane_gather/bf16/RP2"),
+    # fewer than eight images: general kernels
+    ((0, 4, 384, 14, 14, 31), "gen_gather/f32/nchw/RP4"),
     # planes too large for the strip tiles
     ((0, 1, 2, 224, 224, 31), "gen_gather/f32/nchw/RP8"),
 ])
