@@ -179,3 +179,32 @@ def bwd_weight(x, dy, theta_deg, K: int, threads: int | None = None, stride: int
     else:
         lib.oracle_bwd_weight_ex(_ptr(x), _ptr(dy), _ptr(th), _ptr(dw), N, C, H, W, K, stride, MODES[mode], t)
     return dw
+
+
+# ---------------------------------------------------------------- depthwise separable block
+
+def dsc_fwd(x, w_dw, theta_deg, w_pw, threads: int | None = None) -> tuple[np.ndarray, np.ndarray]:
+    """Oriented 1D depthwise separable convolution (Sec. 3.2, "Computational cost analysis", and Table 1's
+    "Oriented 1D DSC" row): the oriented depthwise convolution z = fwd(x, w_dw, theta) followed by the
+    pointwise (1 x 1) convolution y[n,o] = sum_c w_pw[o,c] z[n,c] that mixes C channels into C' = w_pw.shape[0].
+    Returns (z, y)."""
+    w_pw = _f64(w_pw)
+    z = fwd(x, w_dw, theta_deg, threads)
+    if w_pw.ndim != 2 or w_pw.shape[1] != z.shape[1]:
+        raise ValueError(f"w_pw {w_pw.shape} must be (C', C) with C = {z.shape[1]}")
+    y = np.tensordot(w_pw, z, axes=([1], [1])).transpose(1, 0, 2, 3)  # (C', N, H, W) -> (N, C', H, W)
+    return z, np.ascontiguousarray(y)
+
+
+def dsc_bwd(x, dy, w_dw, theta_deg, w_pw, threads: int | None = None):
+    """Gradients of the block: with z the depthwise output, dz[n,c] = sum_o w_pw[o,c] dy[n,o],
+    dw_pw[o,c] = sum_{n,h,w} dy[n,o,h,w] z[n,c,h,w], and (dx, dw_dw) the depthwise convolution's gradients
+    for dz.  Returns (dx, dw_dw, dw_pw)."""
+    w_pw = _f64(w_pw); dy = _f64(dy)
+    K = np.asarray(w_dw).shape[1]
+    z = fwd(x, w_dw, theta_deg, threads)
+    dz = np.ascontiguousarray(np.tensordot(w_pw, dy, axes=([0], [1])).transpose(1, 0, 2, 3))
+    dw_pw = np.tensordot(dy, z, axes=([0, 2, 3], [0, 2, 3]))
+    dx = bwd_input(dz, w_dw, theta_deg, threads)
+    dw_dw = bwd_weight(x, dz, theta_deg, K, threads)
+    return dx, dw_dw, dw_pw
