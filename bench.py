@@ -46,6 +46,7 @@ THETA_TEXT = {
     "zero": "theta = 0 for every channel",
     "ninety": "theta = 90 deg for every channel",
     "ramp": "theta_c = 22.5 c deg",
+    "groups:4": "four equal channel groups at 0, 45, 90, 135 deg",
 }
 
 

@@ -107,10 +107,10 @@ o1d_status_t o1d_bwd_weight(const void* x, const void* dy, const float* theta_de
 
 /* Both gradients of Eq. (1) in one call: dx as o1d_bwd_input computes it
  * (from dy and w) and dw as o1d_bwd_weight computes it (from x and dy).
- * Where the sizes allow (K <= 31, W a multiple of 4, x, dy and dx aligned
- * to 16 bytes for O1D_F32 or 8 bytes for O1D_BF16, planes whose zero-padded
- * tile fits in LDS) one kernel reads x and dy once and produces both; otherwise
- * the kernels of the two separate entry points run in turn.  The results
+ * One kernel reads x and dy once and produces both (then a small kernel adds
+ * the weight gradient's partial rows); only where no one-pass kernel's LDS
+ * tile fits (very large K with very wide planes) do the kernels of the two
+ * separate entry points run in turn.  The results
  * equal those of the separate calls up to the order of floating-point
  * additions and are bitwise reproducible for the same inputs.  dx and dw
  * are overwritten.  `workspace` follows the rules of o1d_bwd_weight and
@@ -173,6 +173,34 @@ o1d_status_t o1d_bwd_weight_ex(const void* x, const void* dy, const float* theta
                                void* workspace, size_t workspace_bytes, void* stream);
 size_t o1d_bwd_weight_ex_workspace_bytes(int N, int C, int H, int W, int K, int stride, o1d_layout_t layout,
                                          o1d_sampling_t sampling, o1d_dtype_t dtype);
+
+/* ---- Oriented 1D depthwise separable block (Sec. 3.2 "Computational cost
+ * analysis", Table 1 "Oriented 1D DSC").
+ *
+ * The oriented depthwise convolution of Eq. (1) (stride 1, NCHW, offsets
+ * rounded down) followed by a pointwise (1 x 1) convolution that mixes the C
+ * channels into Cout:
+ *   z = o1d_fwd(x, w_dw, theta_deg)                       (N x C x H x W)
+ *   y[n,o,h,w] = sum_c w_pw[o,c] z[n,c,h,w]               (N x Cout x H x W)
+ * w_dw is [C][K], w_pw [Cout][C] (row-major), theta_deg [C] float32; x, z, y,
+ * w_dw and w_pw have `dtype` storage.  o1d_dsc_fwd writes z (kept for the
+ * backward) and y; the pointwise product runs on the matrix cores (float32
+ * products for O1D_F32, bfloat16 products for O1D_BF16, float32 accumulation).
+ * o1d_dsc_bwd computes, for the upstream gradient dy (N x Cout x H x W):
+ *   dz = w_pw^T dy (per pixel),  dw_pw[o,c] = sum_{n,h,w} dy[n,o,h,w] z[n,c,h,w],
+ *   (dx, dw_dw) = o1d_bwd(x, dz, w_dw, theta_deg),
+ * with dz kept in `workspace` (at least o1d_dsc_bwd_workspace_bytes(...)
+ * bytes of caller-owned device memory, contents ignored and clobbered); its z
+ * must be the forward's.  dw_pw's images are summed in groups whose float32
+ * partial sums are added in a fixed order (bitwise reproducible).  Outputs
+ * are overwritten; no output may overlap an input, another output or the
+ * workspace.  Cout is 1 .. 65535; other rules as o1d_fwd and o1d_bwd. */
+o1d_status_t o1d_dsc_fwd(const void* x, const void* w_dw, const float* theta_deg, const void* w_pw, void* z,
+                         void* y, int N, int C, int Cout, int H, int W, int K, o1d_dtype_t dtype, void* stream);
+o1d_status_t o1d_dsc_bwd(const void* x, const void* z, const void* dy, const void* w_dw, const float* theta_deg,
+                         const void* w_pw, void* dx, void* dw_dw, void* dw_pw, int N, int C, int Cout, int H,
+                         int W, int K, o1d_dtype_t dtype, void* workspace, size_t workspace_bytes, void* stream);
+size_t o1d_dsc_bwd_workspace_bytes(int N, int C, int Cout, int H, int W, int K, o1d_dtype_t dtype);
 
 /* ---- Planning introspection (host only, no device work; for tests and tools).
  *

@@ -30,6 +30,9 @@ SIGNATURES = {
     "o1d_bwd_input_ex": (_i, [_vp, _vp, _vp, _vp, _i, _i, _i, _i, _i, _i, _i, _i, _i, _vp]),
     "o1d_bwd_weight_ex": (_i, [_vp, _vp, _vp, _vp, _i, _i, _i, _i, _i, _i, _i, _i, _i, _vp, _sz, _vp]),
     "o1d_bwd_weight_ex_workspace_bytes": (_sz, [_i, _i, _i, _i, _i, _i, _i, _i, _i]),
+    "o1d_dsc_fwd": (_i, [_vp, _vp, _vp, _vp, _vp, _vp, _i, _i, _i, _i, _i, _i, _i, _vp]),
+    "o1d_dsc_bwd": (_i, [_vp, _vp, _vp, _vp, _vp, _vp, _vp, _vp, _vp, _i, _i, _i, _i, _i, _i, _i, _vp, _sz, _vp]),
+    "o1d_dsc_bwd_workspace_bytes": (_sz, [_i, _i, _i, _i, _i, _i, _i]),
     "o1d_kernel_name": (ctypes.c_char_p, [_i, _i, _i, _i, _i, _i, _i, _i, _i, _i, _i]),
     "o1d_kernel_variant": (ctypes.c_char_p, [_i]),
     "o1d_status_str": (ctypes.c_char_p, [_i]),

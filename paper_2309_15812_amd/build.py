@@ -44,7 +44,7 @@ def sources() -> list[str]:
 # scratch memory would cost far more than it saves, so their translation
 # units are compiled with resource remarks and rejected if any kernel in them
 # uses scratch memory.  The general kernels are checked the same way.
-CHECKED = ("o1d_strip_", "o1d_gen_", "o1d_plane_")
+CHECKED = ("o1d_strip_", "o1d_gen_", "o1d_plane_", "o1d_pw_")
 REMARK = "-Rpass-analysis=kernel-resource-usage"
 
 

@@ -12,19 +12,23 @@
 //    plane, for a group of images, fits in LDS (lanes over images; any
 //    stride, both discretisations, the fused backward at stride 1 rounding
 //    down);
-//  * general kernels (o1d_gen*.h): everything else the ABI accepts.
+//  * general kernels (o1d_gen*.h): everything else the ABI accepts;
+//  * the depthwise separable block adds the pointwise convolution's matrix
+//    products on the matrix cores (o1d_pw*.h).
 #include <hip/hip_runtime.h>
 #include <stdarg.h>
 #include <stdint.h>
 #include <stdio.h>
 #include <string.h>
 
+#include <algorithm>
 #include <mutex>
 
 #include "o1d.h"
 #include "o1d_gen.h"
 #include "o1d_launch.h"
 #include "o1d_plane.h"
+#include "o1d_pw.h"
 #include "o1d_strip.h"
 
 namespace {
@@ -290,6 +294,68 @@ o1d_status_t bwd_entry(const char* fn, const void* x, const void* dy, const void
 }
 
 
+// ---- depthwise separable block: the pointwise convolution's products
+
+enum PwKind { kPwFwd = 0, kPwDgrad = 1, kPwWgrad = 2 };
+
+// The strided batched product of one pointwise step (see o1d_pw.h); the
+// weight gradient sums the images in groups sized so that about 1024
+// workgroups run.
+o1d::pw::Params pw_params(int kind, int N, int C, int Cout, int H, int W) {
+  o1d::pw::Params p{};
+  const int HW = H * W;
+  p.nbatch = N;
+  if (kind == kPwFwd) {  // Y_n = Wp Z_n
+    p.M = Cout; p.N = HW; p.K = C;
+    p.sA = 0; p.am = C; p.ak = 1; p.a_kc = 1;
+    p.sB = (long long)C * HW; p.bk = HW; p.bn = 1; p.b_nc = 1;
+    p.sC = (long long)Cout * HW; p.cm = HW; p.cn = 1;
+  } else if (kind == kPwDgrad) {  // dZ_n = Wp^T dY_n
+    p.M = C; p.N = HW; p.K = Cout;
+    p.sA = 0; p.am = 1; p.ak = C; p.a_kc = 0;
+    p.sB = (long long)Cout * HW; p.bk = HW; p.bn = 1; p.b_nc = 1;
+    p.sC = (long long)C * HW; p.cm = HW; p.cn = 1;
+  } else {  // dWp = sum_n dY_n Z_n^T
+    p.M = Cout; p.N = C; p.K = HW;
+    p.sA = (long long)Cout * HW; p.am = HW; p.ak = 1; p.a_kc = 1;
+    p.sB = (long long)C * HW; p.bk = 1; p.bn = HW; p.b_nc = 0;
+    p.sC = 0; p.cm = C; p.cn = 1;
+    p.sum = 1;
+  }
+  p.tm = o1d::pw::cdiv(p.M, o1d::pw::kBM);
+  p.tn = o1d::pw::cdiv(p.N, o1d::pw::kBN);
+  if (p.sum) {
+    const int tiles = p.tm * p.tn;
+    int nsplit = std::min(N, std::max(1, o1d::pw::cdiv(1024, tiles)));
+    p.per_split = o1d::pw::cdiv(N, nsplit);
+    p.nsplit = o1d::pw::cdiv(N, p.per_split);
+  }
+  return p;
+}
+
+size_t align256(size_t b) { return (b + 255) & ~(size_t)255; }
+
+// The backward's workspace: dz, the pointwise weight gradient's partials,
+// the depthwise backward's workspace.
+struct DscWorkspace {
+  size_t dz = 0, part = 0, dw = 0, total = 0;
+};
+
+DscWorkspace dsc_workspace(int N, int C, int Cout, int H, int W, int K, o1d_dtype_t dt) {
+  DscWorkspace ws;
+  const o1d::pw::Params pg = pw_params(kPwWgrad, N, C, Cout, H, W);
+  ws.dz = align256(in_elems(N, C, H, W) * elem_size(dt));
+  ws.part = align256((size_t)pg.nsplit * Cout * C * sizeof(float));
+  ws.dw = wgrad_workspace(N, C, H, W, K, dt, Opts());
+  ws.total = ws.dz + ws.part + ws.dw;
+  return ws;
+}
+
+o1d_status_t check_cout(const char* fn, int Cout) {
+  if (Cout < 1 || Cout > 65535) return fail(O1D_ERR_INVALID, "%s: Cout=%d must be 1 .. 65535", fn, Cout);
+  return O1D_OK;
+}
+
 // ---- fixed scratch of the no-allocation entry point (o1d_bwd_noalloc)
 //
 // The weight gradient's partial rows live in a file-scope device array
@@ -414,6 +480,85 @@ o1d_status_t o1d_bwd_noalloc(const void* x, const void* dy, const void* w, const
   st = scratch_ptr(fn, &ptr);
   if (st != O1D_OK) return st;
   return bwd_entry(fn, x, dy, w, theta_deg, dx, dw, N, C, H, W, K, dtype, ptr, kScratchBytes, stream);
+}
+
+o1d_status_t o1d_dsc_fwd(const void* x, const void* w_dw, const float* theta_deg, const void* w_pw, void* z,
+                         void* y, int N, int C, int Cout, int H, int W, int K, o1d_dtype_t dtype, void* stream) {
+  const char* fn = "o1d_dsc_fwd";
+  const Opts o;
+  o1d_status_t st = check_sizes(fn, N, C, H, W, K, dtype, o);
+  if (st != O1D_OK) return st;
+  if ((st = check_cout(fn, Cout)) != O1D_OK) return st;
+  const size_t pix = (size_t)N * H * W;
+  if (pix == 0) return ok();
+  hipStream_t s = static_cast<hipStream_t>(stream);
+  const size_t yb = pix * Cout * elem_size(dtype), zb = in_elems(N, C, H, W) * elem_size(dtype);
+  if (!y) return fail(O1D_ERR_INVALID, "%s: NULL y pointer", fn);
+  (void)hipGetLastError();
+  if (C == 0) return hip_status(fn, o1d::launch_zero((o1d::Dtype)dtype, y, pix * Cout, s));
+  if (!x || !w_dw || !theta_deg || !w_pw || !z) return fail(O1D_ERR_INVALID, "%s: NULL tensor pointer", fn);
+  const size_t xb = zb, wpb = (size_t)Cout * C * elem_size(dtype);
+  if (overlaps(y, yb, x, xb) || overlaps(y, yb, z, zb) || overlaps(y, yb, w_pw, wpb) || overlaps(z, zb, w_pw, wpb))
+    return fail(O1D_ERR_INVALID, "%s: y or z overlaps another tensor", fn);
+  st = gather_entry(fn, x, w_dw, theta_deg, z, N, C, H, W, K, dtype, o, stream, +1);
+  if (st != O1D_OK) return st;
+  return hip_status(fn, o1d::launch_pw_gemm((o1d::Dtype)dtype, pw_params(kPwFwd, N, C, Cout, H, W), w_pw, z, y, s));
+}
+
+size_t o1d_dsc_bwd_workspace_bytes(int N, int C, int Cout, int H, int W, int K, o1d_dtype_t dtype) {
+  const Opts o;
+  if (check_sizes("o1d_dsc_bwd_workspace_bytes", N, C, H, W, K, dtype, o) != O1D_OK) return 0;
+  if (check_cout("o1d_dsc_bwd_workspace_bytes", Cout) != O1D_OK) return 0;
+  if (in_elems(N, C, H, W) == 0) return 0;
+  return dsc_workspace(N, C, Cout, H, W, K, dtype).total;
+}
+
+o1d_status_t o1d_dsc_bwd(const void* x, const void* z, const void* dy, const void* w_dw, const float* theta_deg,
+                         const void* w_pw, void* dx, void* dw_dw, void* dw_pw, int N, int C, int Cout, int H,
+                         int W, int K, o1d_dtype_t dtype, void* workspace, size_t workspace_bytes, void* stream) {
+  const char* fn = "o1d_dsc_bwd";
+  const Opts o;
+  o1d_status_t st = check_sizes(fn, N, C, H, W, K, dtype, o);
+  if (st != O1D_OK) return st;
+  if ((st = check_cout(fn, Cout)) != O1D_OK) return st;
+  if (C == 0) return ok();
+  if (!dw_dw || !dw_pw) return fail(O1D_ERR_INVALID, "%s: NULL weight-gradient pointer", fn);
+  hipStream_t s = static_cast<hipStream_t>(stream);
+  (void)hipGetLastError();
+  const size_t elems = in_elems(N, C, H, W);
+  if (elems == 0) {
+    st = hip_status(fn, o1d::launch_zero((o1d::Dtype)dtype, dw_dw, (size_t)C * K, s));
+    if (st != O1D_OK) return st;
+    return hip_status(fn, o1d::launch_zero((o1d::Dtype)dtype, dw_pw, (size_t)Cout * C, s));
+  }
+  if (!x || !z || !dy || !w_dw || !theta_deg || !w_pw || !dx) return fail(O1D_ERR_INVALID, "%s: NULL tensor pointer", fn);
+  const DscWorkspace ws = dsc_workspace(N, C, Cout, H, W, K, dtype);
+  if (workspace_bytes < ws.total || !workspace)
+    return fail(O1D_ERR_WORKSPACE, "%s: workspace of %zu bytes given, %zu needed", fn, workspace_bytes, ws.total);
+  const size_t es = elem_size(dtype), tb = elems * es, yb = (size_t)N * Cout * H * W * es;
+  const size_t wpb = (size_t)Cout * C * es, wdb = (size_t)C * K * es;
+  const void* ins[] = {x, z, dy, w_dw, w_pw};
+  const size_t inb[] = {tb, tb, yb, wdb, wpb};
+  void* outs[] = {dx, dw_dw, dw_pw, workspace};
+  const size_t outb[] = {tb, wdb, wpb, ws.total};
+  for (int i = 0; i < 4; ++i) {
+    for (int j = 0; j < 5; ++j)
+      if (overlaps(outs[i], outb[i], ins[j], inb[j])) return fail(O1D_ERR_INVALID, "%s: an output overlaps an input", fn);
+    for (int j = i + 1; j < 4; ++j)
+      if (overlaps(outs[i], outb[i], outs[j], outb[j])) return fail(O1D_ERR_INVALID, "%s: outputs overlap", fn);
+  }
+  unsigned char* wsb = static_cast<unsigned char*>(workspace);
+  void* dz = wsb;
+  float* part = reinterpret_cast<float*>(wsb + ws.dz);
+  void* dws = wsb + ws.dz + ws.part;
+  st = hip_status(fn, o1d::launch_pw_gemm((o1d::Dtype)dtype, pw_params(kPwDgrad, N, C, Cout, H, W), w_pw, dy, dz, s));
+  if (st != O1D_OK) return st;
+  const o1d::pw::Params pg = pw_params(kPwWgrad, N, C, Cout, H, W);
+  st = hip_status(fn, o1d::launch_pw_gemm((o1d::Dtype)dtype, pg, dy, z, part, s));
+  if (st != O1D_OK) return st;
+  st = hip_status(fn, o1d::launch_partial_sum((o1d::Dtype)dtype, part, dw_pw, Cout * C, pg.nsplit, s));
+  if (st != O1D_OK) return st;
+  return bwd_entry(fn, x, dz, w_dw, theta_deg, dx, dw_dw, N, C, H, W, K, dtype, dws, ws.dw, stream);
 }
 
 const char* o1d_kernel_name(int op, int N, int C, int H, int W, int K, int stride, o1d_layout_t layout,

@@ -229,3 +229,53 @@ class OrientedConv1dFunction(torch.autograd.Function):
         gx = bwd_input(gy, w, theta) if ctx.needs_input_grad[0] else None
         gw = bwd_weight(x, gy, theta, w.shape[1]) if ctx.needs_input_grad[1] else None
         return gx, gw, None
+
+
+# ---------------------------------------------------------------- depthwise separable block
+
+def _check_pw(w_pw: torch.Tensor, like: torch.Tensor, C: int) -> int:
+    if w_pw.dim() != 2 or w_pw.shape[1] != C or w_pw.dtype != like.dtype:
+        raise ValueError(f"w_pw must be (C', {C}) of dtype {like.dtype}, got {tuple(w_pw.shape)} {w_pw.dtype}")
+    if not w_pw.is_cuda or not w_pw.is_contiguous():
+        raise ValueError("tensors must be contiguous and on the GPU")
+    return int(w_pw.shape[0])
+
+
+def dsc_fwd(x: torch.Tensor, w_dw: torch.Tensor, theta: torch.Tensor, w_pw: torch.Tensor,
+            out: tuple[torch.Tensor, torch.Tensor] | None = None) -> tuple[torch.Tensor, torch.Tensor]:
+    """(z, y): z the oriented depthwise convolution of x, y = w_pw mixing z's channels (Sec. 3.2, Table 1)."""
+    N, C, H, W, K = _check_common(x, w_dw, theta)
+    Co = _check_pw(w_pw, x, C)
+    z, y = (_out(None, x), _out(None, x, (N, Co, H, W))) if out is None else \
+        (_out(out[0], x), _out(out[1], x, (N, Co, H, W)))
+    _lib.check("o1d_dsc_fwd", _lib.call("o1d_dsc_fwd", x.data_ptr(), w_dw.data_ptr(), theta.data_ptr(),
+                                        w_pw.data_ptr(), z.data_ptr(), y.data_ptr(), N, C, Co, H, W, K, _dt(x),
+                                        _stream(x)))
+    return z, y
+
+
+def dsc_workspace_bytes(N: int, C: int, Co: int, H: int, W: int, K: int, dtype: torch.dtype) -> int:
+    return int(_lib.lib().o1d_dsc_bwd_workspace_bytes(N, C, Co, H, W, K, _DT[dtype]))
+
+
+def dsc_bwd(x: torch.Tensor, z: torch.Tensor, dy: torch.Tensor, w_dw: torch.Tensor, theta: torch.Tensor,
+            w_pw: torch.Tensor, out: tuple[torch.Tensor, torch.Tensor, torch.Tensor] | None = None,
+            workspace: torch.Tensor | None = None) -> tuple[torch.Tensor, torch.Tensor, torch.Tensor]:
+    """(dx, dw_dw, dw_pw) of the block given x, the forward's z and dy."""
+    N, C, H, W, K = _check_common(x, w_dw, theta)
+    Co = _check_pw(w_pw, x, C)
+    if z.shape != x.shape or z.dtype != x.dtype or dy.shape != (N, Co, H, W) or dy.dtype != x.dtype:
+        raise ValueError("z must match x, dy must be (N, C', H, W) of x's dtype")
+    for t in (z, dy):
+        if not t.is_cuda or not t.is_contiguous():
+            raise ValueError("tensors must be contiguous and on the GPU")
+    if out is None:
+        dx, dwd, dwp = _out(None, x), _out(None, w_dw), _out(None, w_pw)
+    else:
+        dx, dwd, dwp = _out(out[0], x), _out(out[1], w_dw), _out(out[2], w_pw)
+    workspace, nbytes = _workspace(workspace, x, dsc_workspace_bytes(N, C, Co, H, W, K, x.dtype))
+    _lib.check("o1d_dsc_bwd", _lib.call("o1d_dsc_bwd", x.data_ptr(), z.data_ptr(), dy.data_ptr(), w_dw.data_ptr(),
+                                        theta.data_ptr(), w_pw.data_ptr(), dx.data_ptr(), dwd.data_ptr(),
+                                        dwp.data_ptr(), N, C, Co, H, W, K, _dt(x), workspace.data_ptr(), nbytes,
+                                        _stream(x)))
+    return dx, dwd, dwp

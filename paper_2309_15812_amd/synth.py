@@ -64,6 +64,8 @@ WORKLOADS = {
     "c5": Workload("c5", 32, 256, 56, 56, 31, "f32", "uniform", "fwd+bwd", 4),
     # The headline measurement: stage-1 shape, forward + both gradients.
     "metric": Workload("metric", 64, 96, 56, 56, 31, "f32", "discrete8", "fwd+bwd", 1),
+    # The depthwise separable block of Table 1 (C' = C = 512), four angle groups.
+    "dsc": Workload("dsc", 64, 512, 56, 56, 31, "f32", "groups:4", "fwd+bwd", 5),
 }
 
 
@@ -118,6 +120,22 @@ def make_inputs(wl: Workload, seed: Optional[int] = None, planes: Optional[int] 
     out = {"x": x, "dy": dy, "w": w, "theta": theta}
     if wl.dtype == "bf16":
         for k in ("x", "dy", "w"):
+            bits = to_bf16_bits(out[k])
+            out[k + "_bits"] = bits
+            out[k] = bf16_bits_to_f32(bits)
+    return out
+
+
+def make_pointwise(wl: Workload, cout: int, seed: Optional[int] = None, planes: Optional[int] = None) -> dict:
+    """Draw the depthwise separable block's extra tensors: pointwise weights 'w_pw' (cout, C) ~ N(0, 1/C) and
+    the block's upstream gradient 'dy_pw' (N, cout, H, W) ~ N(0, 1), float32 (bfloat16-rounded values and
+    '*_bits' for bf16 workloads, as make_inputs)."""
+    rng = np.random.default_rng(BASE_SEED + 1000 + wl.seed_index if seed is None else seed)
+    N = wl.N if planes is None else min(wl.N, planes)
+    out = {"w_pw": (rng.standard_normal((cout, wl.C)) / np.sqrt(wl.C)).astype(np.float32),
+           "dy_pw": rng.standard_normal((N, cout, wl.H, wl.W), dtype=np.float32)}
+    if wl.dtype == "bf16":
+        for k in ("w_pw", "dy_pw"):
             bits = to_bf16_bits(out[k])
             out[k + "_bits"] = bits
             out[k] = bf16_bits_to_f32(bits)
