@@ -79,7 +79,8 @@ def parse():
     ap.add_argument("--cpu-seconds", type=float, default=12.0, help="target CPU work for the oracle sample")
     ap.add_argument("--only", default="", help="profiling aid: run only this op (fwd|bwd|bwd_input|bwd_weight), or "
                     "'copy': a plain elementwise copy of one N*C*H*W tensor (reads T bytes, writes T bytes), "
-                    "the calibration kernel for the HBM byte counters")
+                    "the calibration kernel for the HBM byte counters, or dsc_fwd|dsc_bwd: the depthwise "
+                    "separable block at its Table 1 shape")
     return ap.parse_args()
 
 
@@ -215,6 +216,98 @@ def op_stats(case, durs):
     return out
 
 
+MFMA_F32_PEAK_TFLOPS = 157.3  # MI355X dense float32 matrix-core peak
+
+
+class DscSet:
+    """Device buffers of the depthwise separable block (Table 1 shape) for one rotating set."""
+
+    def __init__(self, d, p, torch, dev, ops, cout, dtype):
+        wl_dt = torch.float32 if dtype == "f32" else torch.bfloat16
+        self.x = torch.from_numpy(d["x"]).to(dev).to(wl_dt)
+        self.w = torch.from_numpy(d["w"]).to(dev).to(wl_dt)
+        self.th = torch.from_numpy(d["theta"]).to(dev)
+        self.w_pw = torch.from_numpy(p["w_pw"]).to(dev).to(wl_dt)
+        self.dy = torch.from_numpy(p["dy_pw"]).to(dev).to(wl_dt)
+        N, C, H, W = self.x.shape
+        self.z = torch.empty_like(self.x)
+        self.y = torch.empty((N, cout, H, W), dtype=wl_dt, device=dev)
+        self.dx = torch.empty_like(self.x)
+        self.dwd = torch.empty_like(self.w)
+        self.dwp = torch.empty_like(self.w_pw)
+        self.ws = torch.empty(max(1, ops.dsc_workspace_bytes(N, C, cout, H, W, self.w.shape[1], wl_dt)),
+                              dtype=torch.uint8, device=dev)
+        self.y_dw = torch.empty_like(self.x)
+
+
+def run_dsc(ops, b, name):
+    if name == "dsc_fwd":
+        ops.dsc_fwd(b.x, b.w, b.th, b.w_pw, out=(b.z, b.y))
+    elif name == "dsc_bwd":
+        ops.dsc_bwd(b.x, b.z, b.dy, b.w, b.th, b.w_pw, out=(b.dx, b.dwd, b.dwp), workspace=b.ws)
+    elif name == "dw_fwd":
+        ops.fwd(b.x, b.w, b.th, out=b.y_dw)
+    else:
+        raise ValueError(name)
+
+
+def time_dsc(wl, names, steps, warmup, nsets, torch, ops, synth):
+    """(ms_per_step, {op: [ms]}) for the depthwise separable block at workload wl (C' = C)."""
+    dev = torch.device("cuda:0")
+    sets = []
+    for i in range(nsets):
+        d = synth.make_inputs(wl, seed=synth.BASE_SEED + 500 + i)
+        p = synth.make_pointwise(wl, wl.C, seed=synth.BASE_SEED + 600 + i)
+        sets.append(DscSet(d, p, torch, dev, ops, wl.C, wl.dtype))
+        del d, p
+    for i in range(warmup):
+        for nm in names:
+            run_dsc(ops, sets[i % nsets], nm)
+    stream = torch.cuda.current_stream(dev)
+    ev = []
+
+    def mark():
+        e = torch.cuda.Event(enable_timing=True)
+        e.record(stream)
+        ev.append(e)
+
+    torch.cuda.synchronize()
+    t0 = time.perf_counter()
+    for i in range(steps):
+        for nm in names:
+            mark()
+            run_dsc(ops, sets[i % nsets], nm)
+    mark()
+    torch.cuda.synchronize()
+    t1 = time.perf_counter()
+    durs = {nm: [ev[i * len(names) + j].elapsed_time(ev[i * len(names) + j + 1]) for i in range(steps)]
+            for j, nm in enumerate(names)}
+    del sets
+    torch.cuda.empty_cache()
+    return (t1 - t0) * 1e3 / steps, durs
+
+
+def dsc_stats(wl, ms, durs):
+    """The block's per-op times and the pointwise product's estimated matrix-core rate: its share of the
+    forward pass is the forward minus the depthwise forward alone (the same shape, timed beside it)."""
+    mean = {k: statistics.fmean(v) for k, v in durs.items()}
+    flop = 2.0 * wl.N * wl.H * wl.W * wl.C * wl.C  # one pointwise product (C' = C)
+    pw_ms = mean["dsc_fwd"] - mean["dw_fwd"]
+    tflops = flop / (pw_ms * 1e-3) / 1e12 if pw_ms > 0 else None
+    return {
+        "workload": f"{wl.N}x{wl.C}->{wl.C}x{wl.H}x{wl.W} K={wl.K} {wl.dtype}, "
+                    f"{THETA_TEXT.get(wl.theta, wl.theta)} (Table 1's block shape)",
+        "ms_per_step": round(ms, 4),
+        "ops_ms": {k: round(v, 4) for k, v in mean.items()},
+        "pointwise_flop_per_product": flop,
+        "pointwise_fwd_ms_est": round(pw_ms, 4),
+        "pointwise_tflops_est": None if tflops is None else round(tflops, 1),
+        "mfma_peak_tflops": MFMA_F32_PEAK_TFLOPS if wl.dtype == "f32" else 2500.0,
+        "mfma_frac_est": None if tflops is None else round(
+            tflops / (MFMA_F32_PEAK_TFLOPS if wl.dtype == "f32" else 2500.0), 4),
+    }
+
+
 def algorithmic_bytes(wl) -> dict:
     """Bytes each op of the plain (stride 1, NCHW) path must move (T = one N*C*H*W tensor): the forward
     reads x and writes y; the fused backward reads x and dy and writes dx and dw; the separate gradients
@@ -296,6 +389,13 @@ def main():
 
     from paper_2309_15812_amd import ops, synth
 
+    if args.only in ("dsc_fwd", "dsc_bwd"):
+        # profiling aid: the depthwise separable block at its Table 1 shape
+        dwl = synth.WORKLOADS["dsc"]
+        m, dd = time_dsc(dwl, [args.only], args.steps, args.warmup, 2, torch, ops, synth)
+        print(json.dumps({"only": args.only, "ms_per_step": round(m, 5),
+                          "ms_mean": round(statistics.fmean(dd[args.only]), 5)}), flush=True)
+        return
     wl = synth.WORKLOADS[args.workload]
     head = Case(wl)
     T = wl.elems * wl.elem_bytes
@@ -384,6 +484,11 @@ def main():
             sweep[f"K{K}"] = {**res, "max_over_theta0_step": round(r_step, 3), "max_over_theta0_fwd": round(r_fwd, 3)}
             print(f"[bench] angle sweep K={K}: {sweep[f'K{K}']}", file=sys.stderr, flush=True)
         out["angle_cost"] = {"workload": "32x256x56x56 f32 fwd+bwd", **sweep}
+        # the depthwise separable block (Sec. 3.2, Table 1): depthwise + pointwise on the matrix cores
+        dwl = W["dsc"]
+        m, dd = time_dsc(dwl, ["dsc_fwd", "dsc_bwd", "dw_fwd"], 10, 3, 2, torch, ops, synth)
+        out["dsc_block"] = dsc_stats(dwl, m, dd)
+        print(f"[bench] dsc block: {out['dsc_block']}", file=sys.stderr, flush=True)
 
     if not args.no_cpu and not args.only:
         print("[bench] timing the CPU oracle ...", file=sys.stderr, flush=True)
