@@ -57,38 +57,19 @@ struct Cells {
   }
 };
 
-// Builds the cell tables of channels c0 .. c0 + CB - 1: one thread per
-// (channel, tap) computes the tap's one (rounded down) or up to four
-// (bilinear, corners with a zero coefficient dropped) cells; `scratch` (CB K
-// ints) holds the per-tap cell counts for the prefix sum.  A non-finite angle
-// gives the channel NaN weights and coefficients.
-template <typename T>
-__device__ void build_cells(const Params& P, const Cells& cl, const T* __restrict__ wgt,
-                            const float* __restrict__ theta, int c0, int* scratch) {
-  const int K = P.K, CB = P.CB;
-  const int t = threadIdx.x;
-  // corner s of the tap: (h0 + (s >> 1), w0 + (s & 1)) with coefficient cf[s]
-  // (rounding down: corner 0 only, coefficient 1)
-  double cf[4] = {0.0, 0.0, 0.0, 0.0};
-  int h0 = 0, w0 = 0, n = 0;
-  bool fin = true;
-  const bool act = t < CB * K && c0 + t / K < P.C;
-  if (t < CB) cl.cnt[t] = 0;  // channels past C keep no cells
-  // every slot starts as a dummy cell: offset 0 (the output's own centre,
-  // which tap K/2 reads anyway), weight and coefficient 0, so that groups of
-  // eight cells can run past the last real one
-  for (int j = t; j < CB * cl.ncap; j += kThreads) {
-    cl.cw[2 * j] = 0;
-    cl.cw[2 * j + 1] = 0;
-    cl.tap[j] = 0;
-    cl.coef[j] = 0.f;
-  }
-  if (act) {
-    const int ch = t / K, k = t - ch * K, c = c0 + ch;
+// One tap's cells: corner s at (h0 + (s >> 1), w0 + (s & 1)) with
+// coefficient cf[s] (rounding down: corner 0 only, coefficient 1); n of the
+// four coefficients are non-zero.  fin is false for a non-finite angle.
+struct TapCells {
+  double cf[4];
+  int h0, w0, n;
+  bool fin;
+  __device__ __forceinline__ TapCells(const Params& P, float theta, int k) {
     double rh, rw;
-    fin = tap_real(theta[c], K, k, &rh, &rw);
+    fin = tap_real(theta, P.K, k, &rh, &rw);
     h0 = floor_snapped(rh);
     w0 = floor_snapped(rw);
+    cf[0] = cf[1] = cf[2] = cf[3] = 0.0;
     if (P.mode == 0 || !fin) {
       cf[0] = 1.0;
     } else {
@@ -96,13 +77,39 @@ __device__ void build_cells(const Params& P, const Cells& cl, const T* __restric
 #pragma unroll
       for (int s = 0; s < 4; ++s) cf[s] = ((s >> 1) ? fh : 1.0 - fh) * ((s & 1) ? fw : 1.0 - fw);
     }
+    n = 0;
 #pragma unroll
     for (int s = 0; s < 4; ++s) n += cf[s] != 0.0 ? 1 : 0;
-    scratch[t] = n;
   }
+};
+
+// Builds the cell tables of channels c0 .. c0 + CB - 1: the workgroup's
+// threads take the CB K (channel, tap) pairs in turn; each computes the tap's
+// one (rounded down) or up to four (bilinear, corners with a zero coefficient
+// dropped) cells, once to count them into `scratch` (CB K ints, for the
+// prefix sum) and again to write them.  A non-finite angle gives the channel
+// NaN weights and coefficients.
+template <typename T>
+__device__ void build_cells(const Params& P, const Cells& cl, const T* __restrict__ wgt,
+                            const float* __restrict__ theta, int c0, int* scratch) {
+  const int K = P.K, CB = P.CB;
+  for (int t = threadIdx.x; t < CB; t += kThreads) cl.cnt[t] = 0;  // channels past C keep no cells
+  // every slot starts as a dummy cell: offset 0 (the output's own centre,
+  // which tap K/2 reads anyway), weight and coefficient 0, so that groups of
+  // eight cells can run past the last real one
+  for (int j = threadIdx.x; j < CB * cl.ncap; j += kThreads) {
+    cl.cw[2 * j] = 0;
+    cl.cw[2 * j + 1] = 0;
+    cl.tap[j] = 0;
+    cl.coef[j] = 0.f;
+  }
+  for (int t = threadIdx.x; t < CB * K; t += kThreads)
+    if (c0 + t / K < P.C) scratch[t] = TapCells(P, theta[c0 + t / K], t % K).n;
   __syncthreads();
-  if (act) {
+  for (int t = threadIdx.x; t < CB * K; t += kThreads) {
     const int ch = t / K, k = t - ch * K, c = c0 + ch;
+    if (c >= P.C) continue;
+    const TapCells tc(P, theta[c], k);
     int base = k;  // rounding down: one cell per tap
     if (P.mode != 0) {
       base = 0;
@@ -114,17 +121,17 @@ __device__ void build_cells(const Params& P, const Cells& cl, const T* __restric
     int j = ch * cl.ncap + base;
 #pragma unroll
     for (int s = 0; s < 4; ++s) {
-      if (cf[s] != 0.0) {
-        const int off = P.sign * ((h0 + (s >> 1)) * P.TC + w0 + (s & 1));
-        const float wc = fin ? (float)((double)wk * cf[s]) : __builtin_nanf("");
+      if (tc.cf[s] != 0.0) {
+        const int off = P.sign * ((tc.h0 + (s >> 1)) * P.TC + tc.w0 + (s & 1));
+        const float wc = tc.fin ? (float)((double)wk * tc.cf[s]) : __builtin_nanf("");
         cl.cw[2 * j] = off;
         cl.cw[2 * j + 1] = __float_as_int(wc);
         cl.tap[j] = k;
-        cl.coef[j] = fin ? (float)cf[s] : __builtin_nanf("");
+        cl.coef[j] = tc.fin ? (float)tc.cf[s] : __builtin_nanf("");
         ++j;
       }
     }
-    if (k == K - 1) cl.cnt[ch] = base + n;
+    if (k == K - 1) cl.cnt[ch] = base + tc.n;
   }
   __syncthreads();
 }

@@ -162,8 +162,16 @@ PLANE_EX = [
     (33, 3, 10, 6, 15, "f32", "uniform", 1, "nchw", "floor"),
 ]
 
+# general kernels whose workgroups hold more (channel, tap) pairs than
+# threads (NHWC channel blocks with long kernels): every tap's cells built
+EX_MANY_TAPS = [
+    (2, 16, 14, 14, 63, "bf16", "uniform", 1, "nhwc", "floor"),
+    (2, 8, 9, 9, 127, "f32", "uniform", 1, "nhwc", "floor"),
+    (2, 12, 11, 13, 33, "bf16", "uniform", 2, "nhwc", "bilinear"),
+]
 
-@pytest.mark.parametrize("case", EX + PLANE_EX, ids=lambda c: "-".join(map(str, c)))
+
+@pytest.mark.parametrize("case", EX + PLANE_EX + EX_MANY_TAPS, ids=lambda c: "-".join(map(str, c)))
 def test_stride_layout_sampling(case):
     N, C, H, W, K, dtype, theta, s, layout, sampling = case
     run_ex(N, C, H, W, K, dtype, theta, s, layout, sampling, label=str(case))
