@@ -31,8 +31,8 @@ constexpr size_t kLdsBudget = 64 * 1024;
 
 // Odd tile row strides compiled into the kernels: for an odd stride the
 // transposed staging accesses of a half-wave hit 32 distinct banks.
-#define O1D_STRIP_STRIDES(X) X(47) X(63) X(77) X(87) X(103) X(119) X(143)
-constexpr int kStrides[] = {47, 63, 77, 87, 103, 119, 143};
+#define O1D_STRIP_STRIDES(X) X(47) X(51) X(63) X(77) X(87) X(103) X(119) X(143)
+constexpr int kStrides[] = {47, 51, 63, 77, 87, 103, 119, 143};
 
 __host__ __device__ inline int cdiv(int a, int b) { return (a + b - 1) / b; }
 
@@ -116,7 +116,9 @@ struct Params {
   int G;      // planes staged at once (one task per lane for all of them)
   int npw;    // images per workgroup
   int halo;   // zero rows above and below the plane in the tile
-  int mc;     // zero columns left and right of the plane in the tile
+  int mc;     // columns a walk reads past either side of the plane; the zero gap between
+              // consecutive tile rows (S - max(H, W) >= mc) serves as the right margin of one
+              // row and the left margin of the next
   int TR;     // tile rows
   int PS;     // floats per tile slot, guards included
   int ks, ms; // staging grid per plane: steps of 8 kWaves rows, segments of 32 columns
@@ -142,7 +144,14 @@ inline Plan plan_strip(int N, int C, int H, int W, int K, int sign, int kind, bo
   if (W % 4 != 0 || !vec_ok) return pl;
   const int M = H > W ? H : W;
   const int halo = (K / 2) < (M - 1) ? (K / 2) : (M - 1);
-  const int mc = halo > kRd - 1 + kNd - 1 + 2 ? halo : kRd - 1 + kNd - 1 + 2;
+  // Column reach: the staging frame puts the line's longer extent along its
+  // rows, so a cell's column offset is at most floor((K / 2) sin 45 deg) + 1
+  // in magnitude (checked by enumeration of the offsets of Eq. 2 over
+  // angles, K <= 63; one more here for margin); a diagonal block adds the
+  // R - 1 columns its strips start left of the plane, or its NC - 1 + R - 1
+  // columns past its first strip on the right.
+  const int bmax = (int)((K / 2) * 0.70711) + 2;
+  const int mc = kRd - 1 + kNd - 1 + bmax;
   int cover = 0, ppt = 0;
   for (int f = 0; f < 2; ++f)
     for (int s = 0; s < 2; ++s) {
@@ -150,9 +159,11 @@ inline Plan plan_strip(int N, int C, int H, int W, int K, int sign, int kind, bo
       if (t.nb * t.R > cover) cover = t.nb * t.R;
       if (t.ppt > ppt) ppt = t.ppt;
     }
+  // rows share their margins: the gap of S - M >= mc zero columns after a
+  // row's data is also the left margin of the next row
   int S = 0;
   for (int s : kStrides)
-    if (s >= M + 2 * mc) {
+    if (s >= M + mc) {
       S = s;
       break;
     }
@@ -162,7 +173,10 @@ inline Plan plan_strip(int N, int C, int H, int W, int K, int sign, int kind, bo
   p.halo = halo;
   p.mc = mc;
   p.TR = cover + 2 * halo;
-  p.PS = p.TR * S + 2 * kGuard;
+  // the last row's right-hand reads run up to mc + M + mc - S columns past
+  // the tile
+  const int tail = mc + M + mc - S > kGuard ? mc + M + mc - S : kGuard;
+  p.PS = p.TR * S + kGuard + tail;
   p.ks = cdiv(H, 8 * kWaves);
   p.ms = cdiv(W, 32);
   const int per_plane_slots = p.ks * p.ms;

@@ -22,7 +22,7 @@ def _candidates():
     # strip kernels: W a multiple of 4, aligned tensors, every tile stride
     for K in (7, 31, 33, 63):
         for M in range(4, 132, 4):
-            for H, W in ((M, M), (max(1, M // 3), M), (M, max(4, (M // 3) // 4 * 4))):
+            for H, W in ((M, M), (max(1, M // 3), M), (max(1, M // 4), M), (M, max(4, (M // 3) // 4 * 4))):
                 out.append((3, 4, H, W, K, _lib.O1D_NCHW, True))
     # plane kernels: small NCHW planes with at least eight images
     for K in (7, 31, 63, 127):

@@ -30,12 +30,12 @@ def test_planned_names_are_compiled_variants():
 
 @pytest.mark.parametrize("args,expect", [
     # the headline shape: strip kernels, fused backward
-    ((0, 64, 96, 56, 56, 31), "strip_gather/f32/S87/KB32"),
-    ((3, 64, 96, 56, 56, 31), "strip_bwd/f32/S87/KB32"),
-    ((3, 64, 192, 28, 28, 31), "strip_bwd/f32/S63/KB32"),
+    ((0, 64, 96, 56, 56, 31), "strip_gather/f32/S77/KB32"),
+    ((3, 64, 96, 56, 56, 31), "strip_bwd/f32/S77/KB32"),
+    ((3, 64, 192, 28, 28, 31), "strip_bwd/f32/S51/KB32"),
     # K = 63: strip gather; both gradients in the general one-pass kernel (the
     # strip one stops at 31 cells)
-    ((0, 32, 256, 56, 56, 63), "strip_gather/f32/S119/KB64"),
+    ((0, 32, 256, 56, 56, 63), "strip_gather/f32/S103/KB64"),
     ((3, 32, 256, 56, 56, 63), "gen_bwd/f32/nchw/RP4/KB64"),
     # 14 x 14 planes (W not a multiple of 4) with many images: plane kernels
     # (lanes over images), two rows per lane
@@ -56,7 +56,7 @@ def test_routing_of_options():
     assert _lib.kernel_name(0, 2, 4, 56, 56, 31, 1, _lib.O1D_NHWC).startswith("gen_gather/f32/nhwc")
     assert _lib.kernel_name(2, 2, 4, 56, 56, 31, 1, _lib.O1D_NCHW, _lib.O1D_BILINEAR).startswith("gen_wgrad/")
     assert _lib.kernel_name(0, 2, 4, 56, 56, 31, aligned=False).startswith("gen_gather/")
-    assert _lib.kernel_name(0, 2, 4, 56, 56, 31, dtype=_lib.O1D_BF16) == "strip_gather/bf16/S87/KB32"
+    assert _lib.kernel_name(0, 2, 4, 56, 56, 31, dtype=_lib.O1D_BF16) == "strip_gather/bf16/S77/KB32"
     # invalid or empty sizes name no kernel
     assert _lib.kernel_name(0, 2, 4, 56, 56, 30) == ""
     assert _lib.kernel_name(0, 0, 4, 56, 56, 31) == ""
