@@ -113,7 +113,7 @@ Route route(int op, int N, int C, int H, int W, int K, o1d_dtype_t dt, const Opt
   if (o.plain()) {
     // the fused backward has the weight gradient's strip plan
     r.sp = o1d::strip::plan_strip(N, C, H, W, K, op == kOpDgrad || op == kOpBwd ? -1 : 1,
-                                  op == kOpWgrad || op == kOpBwd ? 1 : 0, aligned);
+                                  op == kOpWgrad ? 1 : (op == kOpBwd ? 2 : 0), aligned);
     if (r.sp.ok) {
       r.ok = true;
       r.fam = Family::Strip;

@@ -135,12 +135,13 @@ struct Plan {
   bool ok = false;
 };
 
-// kind: 0 = gather (forward / input gradient), 1 = weight gradient.
+// kind: 0 = gather (forward / input gradient), 1 = weight gradient, 2 =
+// fused backward (the weight gradient's layout).
 // vec_ok: tensors aligned for 4-element vector accesses.
 inline Plan plan_strip(int N, int C, int H, int W, int K, int sign, int kind, bool vec_ok) {
   Plan pl;
-  if (K < 1 || K > kMaxTaps || N < 1 || C < 1 || H < 1 || W < 1) return pl;
-  if (kind == 1 && K > 32) return pl;  // see launch_wgrad_strip
+  if (K < 1 || K > kMaxTaps || N < 1 || C < 1 || H < 1 || W < 1 || kind < 0 || kind > 2) return pl;
+  if (kind >= 1 && K > 32) return pl;  // see launch_wgrad_strip
   if (W % 4 != 0 || !vec_ok) return pl;
   const int M = H > W ? H : W;
   const int halo = (K / 2) < (M - 1) ? (K / 2) : (M - 1);
@@ -188,7 +189,7 @@ inline Plan plan_strip(int N, int C, int H, int W, int K, int sign, int kind, bo
   if (G * per_plane_slots > max_slots) G = max_slots / per_plane_slots;
   if (G < 1) return pl;
   const int trash = 64 + 3 * S + 4;  // a word per lane plus the reach of a transposed vector write
-  const int red = kind == 1 ? kWaves * 64 : 0;  // weight gradient: per-wave cell sums
+  const int red = kind >= 1 ? kWaves * 64 : 0;  // weight gradients: per-wave cell sums
   auto lds_for = [&](int g) { return ((size_t)kProgWords + (size_t)g * p.PS + (size_t)red + (size_t)trash) * 4; };
   while (G > 1 && lds_for(G) > kLdsBudget) --G;
   if (lds_for(G) > kMaxLdsBytes) return pl;
@@ -198,12 +199,15 @@ inline Plan plan_strip(int N, int C, int H, int W, int K, int sign, int kind, bo
   p.G = G;
   p.nq = G * per_plane_slots;
   p.trash = kProgWords + G * p.PS + red;
-  // images per workgroup: from the LDS rule and about two waves per SIMD;
-  // the gather launcher refits it to the kernel's residency, the weight
-  // gradient keeps it (its workspace size depends on it)
+  // images per workgroup: from the LDS rule and the kernel's registers
+  // (waves per SIMD: the weight gradient's walk keeps 32 cell sums and the
+  // window, two; the fused backward, below 168 registers, three); the
+  // gather launcher refits it to the kernel's residency, the weight
+  // gradients keep it (their workspace size depends on it)
   const size_t lds = lds_for(G);
   int per_cu = lds_resident(lds);
-  if (per_cu > 4) per_cu = 4;
+  const int by_regs = kind == 2 ? 3 * 4 / kWaves : 2 * 4 / kWaves;
+  if (per_cu > by_regs) per_cu = by_regs;
   const int npw = fit_npw(N, C, G, 256LL * (per_cu < 1 ? 1 : per_cu));
   p.npw = npw;
   pl.S = S;

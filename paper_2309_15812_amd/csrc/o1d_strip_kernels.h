@@ -199,6 +199,14 @@ __device__ __forceinline__ float lds_load(uint32_t a) {
 __device__ __forceinline__ void lds_store(uint32_t a, float v) {
   *(__attribute__((address_space(3))) float*)(uintptr_t)a = v;
 }
+// The value of v, opaque to the optimiser.  A loop-invariant LDS base used
+// with constant offsets inside a loop would otherwise be hoisted as one
+// precomputed address per offset (a register each); through this the
+// offsets stay immediates of the accesses.
+__device__ __forceinline__ uint32_t opaque(uint32_t v) {
+  asm volatile("" : "+v"(v));
+  return v;
+}
 
 // The window step of cell C: a run's first cell reloads all R rows, every
 // cell but the walk's last reads the next cell's new row (assuming that cell
@@ -214,10 +222,25 @@ __device__ __forceinline__ void window_step(float (&sl)[R + 1][NC], uint32_t& ba
   asm volatile("" : "+s"(b));
   if (b & (1u << (C & 31))) {
     base = lb + (uint32_t)__builtin_amdgcn_readlane((int)vrb, C);
+    if constexpr (NC == 1) {
+      // One value per row.  Rows i and i + 1 share no base register: loads
+      // from one base within 256 words of each other would be paired into
+      // 64-bit reads, whose destinations must be an even-aligned register
+      // pair, which the rotating rows are not (the pair would land in
+      // temporaries and be copied row by row).  Row i reads through base
+      // i mod kBases; rows on one base are at least 256 words apart.
+      constexpr int kBases = (256 + ST - 1) / ST;
+      uint32_t bb[kBases];
 #pragma unroll
-    for (int i = 0; i < R; ++i)
+      for (int m = 0; m < kBases; ++m) bb[m] = opaque(base);
 #pragma unroll
-      for (int k = 0; k < NC; ++k) sl[(C + i) % (R + 1)][k] = lds_load(base + 4u * (uint32_t)((C + i) * ST + k));
+      for (int i = 0; i < R; ++i) sl[(C + i) % (R + 1)][0] = lds_load(bb[i % kBases] + 4u * (uint32_t)((C + i) * ST));
+    } else {
+#pragma unroll
+      for (int i = 0; i < R; ++i)
+#pragma unroll
+        for (int k = 0; k < NC; ++k) sl[(C + i) % (R + 1)][k] = lds_load(base + 4u * (uint32_t)((C + i) * ST + k));
+    }
   }
   if constexpr (C + 1 < KB) {
 #pragma unroll
@@ -362,8 +385,10 @@ struct BwdWalk<R, NC, ST, KW, KW, KB> {
 //  * goff[q]: byte offset of its 4 elements from the group's first element,
 //    or kOob for a slot outside the plane; buffer accesses beyond the
 //    resource's size read zeros and drop stores;
-//  * lt[q]: LDS address of the first element in the tile (frame orientation),
-//    or of the lane's word in the trash area for a slot outside the plane.
+//  * lt(q): LDS address of the first element in the tile (frame orientation),
+//    or of the lane's word in the trash area for a slot outside the plane;
+//    kept as 16-bit word indices, two slots per register (LDS holds fewer
+//    than 2^16 words), which saves kQ / 2 registers through the walk.
 constexpr uint32_t kOob = 0x80000000u;
 
 template <int NQ, class F>
@@ -426,8 +451,17 @@ template <typename T>
 struct Stage {
   static constexpr int kQ = kMaxSlots;
   static constexpr int kWords = kMaxSlots * Raw<T>::kWords;  // staging registers per group
+  static_assert(kQ % 2 == 0, "slots are packed in pairs");
   uint32_t goff[kQ];
-  uint32_t lt[kQ];
+  uint32_t ltp[kQ / 2];  // word indices: slot 2 i in the low half, slot 2 i + 1 in the high half
+
+  // LDS byte address of slot q's first element.  The packed pair passes
+  // through opaque() so that the unpacking stays next to its use instead
+  // of being hoisted out of the group loop into kQ registers.
+  __device__ __forceinline__ uint32_t lt(int q) const {
+    const uint32_t w = opaque(ltp[q >> 1]);
+    return (q & 1) ? (w >> 16) << 2 : (w & 0xffffu) << 2;
+  }
 
   __device__ __forceinline__ void init_global(const Params& P) {
     const int img = P.C * P.H * P.W;
@@ -436,10 +470,14 @@ struct Stage {
     });
   }
   __device__ __forceinline__ void init_lds(const Params& P, int S, bool tr, uint32_t tiles, uint32_t trash) {
-    const uint32_t tl = trash + 4 * (threadIdx.x & 63);
+    const uint32_t tl = (trash >> 2) + (threadIdx.x & 63);
     for_each_slot<kQ>(P, [&](int q, bool ok, int g, int h, int w) __attribute__((always_inline)) {
       const int r = tr ? w : h, c = tr ? h : w;
-      lt[q] = ok ? tiles + 4 * (uint32_t)(g * P.PS + kGuard + (P.halo + r) * S + P.mc + c) : tl;
+      const uint32_t word = ok ? (tiles >> 2) + (uint32_t)(g * P.PS + kGuard + (P.halo + r) * S + P.mc + c) : tl;
+      if (q & 1)
+        ltp[q >> 1] |= word << 16;
+      else
+        ltp[q >> 1] = word;
     });
   }
   // Loads the group's slots (ng >= 1 planes from src) into raw registers.
@@ -453,20 +491,41 @@ struct Stage {
   }
   // Writes the slots into the tile: the 4 elements of a slot are consecutive
   // along the frame's rows, or along its columns (stride S) when transposed.
-  __device__ __forceinline__ void store_lds(const Params& P, int S, bool tr, const uint32_t (&v)[kWords]) const {
-    const uint32_t step = tr ? 4u * S : 4u;
+  // The frame is uniform, so each branch has a constant step, which the LDS
+  // accesses take as immediate offsets (a runtime step would hold 4 kQ
+  // precomputed addresses in registers).
+  template <int S>
+  __device__ __forceinline__ void store_lds(bool tr, const uint32_t (&v)[kWords]) const {
+    if (tr)
+      store_lds_step<4 * S>(v);
+    else
+      store_lds_step<4>(v);
+  }
+  template <int STEP>
+  __device__ __forceinline__ void store_lds_step(const uint32_t (&v)[kWords]) const {
 #pragma unroll
-    for (int q = 0; q < kQ; ++q)
+    for (int q = 0; q < kQ; ++q) {
+      const uint32_t a = lt(q);
 #pragma unroll
-      for (int j = 0; j < 4; ++j) lds_store(lt[q] + j * step, Raw<T>::elem(&v[Raw<T>::kWords * q], j));
+      for (int j = 0; j < 4; ++j) lds_store(a + j * STEP, Raw<T>::elem(&v[Raw<T>::kWords * q], j));
+    }
   }
   // Reads the tile's outputs (frame orientation) in the slot layout.
-  __device__ __forceinline__ void read_lds(const Params& P, int S, bool tr, float (&e)[kQ][4]) const {
-    const uint32_t step = tr ? 4u * S : 4u;
+  template <int S>
+  __device__ __forceinline__ void read_lds(bool tr, float (&e)[kQ][4]) const {
+    if (tr)
+      read_lds_step<4 * S>(e);
+    else
+      read_lds_step<4>(e);
+  }
+  template <int STEP>
+  __device__ __forceinline__ void read_lds_step(float (&e)[kQ][4]) const {
 #pragma unroll
-    for (int q = 0; q < kQ; ++q)
+    for (int q = 0; q < kQ; ++q) {
+      const uint32_t a = lt(q);
 #pragma unroll
-      for (int j = 0; j < 4; ++j) e[q][j] = lds_load(lt[q] + j * step);
+      for (int j = 0; j < 4; ++j) e[q][j] = lds_load(a + j * STEP);
+    }
   }
   __device__ __forceinline__ void store(const Params& P, T* dst, int ng, const float (&e)[kQ][4]) const {
     const __amdgpu_buffer_rsrc_t rs = buffer_of(dst, ng * P.C * P.H * P.W * (int)sizeof(T));
@@ -575,9 +634,9 @@ __device__ __forceinline__ void gather_groups(const Params& P, const Chan& ch, f
     if (task && g < ng) put_block<R, NC, ST, SD>(bk, ch, acc);
     __syncthreads();  // the group's outputs are in the tile
     float e[Stage<T>::kQ][4];
-    stg.read_lds(P, S, ch.tr != 0, e);
+    stg.template read_lds<S>(ch.tr != 0, e);
     __syncthreads();  // the tile is free
-    stg.store_lds(P, S, ch.tr != 0, pre);  // past the end: zeros into a tile nobody reads
+    stg.template store_lds<S>(ch.tr != 0, pre);  // past the end: zeros into a tile nobody reads
     stg.store(P, outc + (size_t)n0 * img, ng, e);
     __syncthreads();  // the next group is staged
   }
@@ -618,7 +677,7 @@ __global__ __launch_bounds__(kThreads) void strip_gather(Params P, const T* __re
   ch.Hs = ch.tr ? P.W : P.H;
   ch.Ws = ch.tr ? P.H : P.W;
   stg.init_lds(P, S, ch.tr != 0, lds_addr(tiles), lds_addr(smem + P.trash));
-  stg.store_lds(P, S, ch.tr != 0, pre);
+  stg.template store_lds<S>(ch.tr != 0, pre);
   __syncthreads();
   if (ch.s == 0)
     gather_groups<T, S, KB, kRv, kNv, 0>(P, ch, smem, inc, outc, n_begin, n_end, stg, pre);
@@ -647,7 +706,7 @@ __device__ __forceinline__ void wgrad_groups(const Params& P, const Chan& ch, fl
     {
       uint32_t dpre[Stage<T>::kWords];
       stg.load(P, dc + (size_t)n0 * img, min(P.G, n_end - n0), dpre);
-      stg.store_lds(P, S, ch.tr != 0, dpre);
+      stg.template store_lds<S>(ch.tr != 0, dpre);
     }
     __syncthreads();  // dy of the group is in the tile
     float dv[R][NC];
@@ -656,7 +715,7 @@ __device__ __forceinline__ void wgrad_groups(const Params& P, const Chan& ch, fl
 #pragma unroll
       for (int k = 0; k < NC; ++k) dv[i][k] = bk.task ? lds_load(bk.lb + 4 * (i * ST + k)) : 0.f;
     __syncthreads();  // every lane has its dy
-    stg.store_lds(P, S, ch.tr != 0, xpre);
+    stg.template store_lds<S>(ch.tr != 0, xpre);
     __syncthreads();  // x of the group is in the tile
     // the next group's x (past the end: an empty range, see gather_groups)
     const int nn = max(0, min(P.G, n_end - n0 - P.G));
@@ -756,8 +815,8 @@ __global__ __launch_bounds__(kThreads, 2) void strip_wgrad(Params P, const T* __
 // the weight gradient of the cell's taps (Eq. 1 differentiated in w, with
 // the output position moved onto x).  The input gradient leaves through
 // the tile as in gather_groups.  A group's dy is loaded while the lanes
-// copy its x, the next group's x after the walk (no staging registers stay
-// live through the walk, which needs them for the second block).
+// copy its x, the next group's x once the lanes have written their input
+// gradient blocks (no staging registers stay live through the walk).
 template <typename T, int S, int KB, int R, int NC, int SD>
 __device__ __forceinline__ void bwd_groups(const Params& P, const Chan& ch, float* smem, const T* xc, const T* dc,
                                            T* dxc, int n_begin, int n_end, Stage<T>& stg,
@@ -777,7 +836,7 @@ __device__ __forceinline__ void bwd_groups(const Params& P, const Chan& ch, floa
 #pragma unroll
       for (int k = 0; k < NC; ++k) xv[i][k] = bk.task ? lds_load(bk.lb + 4 * (i * ST + k)) : 0.f;
     __syncthreads();  // every lane has its x
-    stg.store_lds(P, S, ch.tr != 0, pre);
+    stg.template store_lds<S>(ch.tr != 0, pre);
     __syncthreads();  // dy of the group is in the tile
     // the next group's x (past the end: an empty range, see gather_groups)
     const int nn = max(0, min(P.G, n_end - n0 - P.G));
@@ -791,14 +850,16 @@ __device__ __forceinline__ void bwd_groups(const Params& P, const Chan& ch, floa
     uint32_t base = bk.lb;
     BwdWalk<R, NC, ST, 0, KB - 1, KB>::run(ch.ncells, base, bk.lb, ch.vrb, ch.bits_lo, ch.bits_hi, ch.vw, sl, xv, out,
                                           acc);
-    stg.load(P, xc + next, nn, pre);
     __syncthreads();  // every lane has finished reading the tile
     if (bk.task && bk.g < ng) put_block<R, NC, ST, SD>(bk, ch, out);
+    // issued once the block is out of registers (in flight next to the
+    // block, the loads would set the kernel's register peak)
+    stg.load(P, xc + next, nn, pre);
     __syncthreads();  // the group's input gradient is in the tile
     float e[Stage<T>::kQ][4];
-    stg.read_lds(P, S, ch.tr != 0, e);
+    stg.template read_lds<S>(ch.tr != 0, e);
     __syncthreads();  // the tile is free
-    stg.store_lds(P, S, ch.tr != 0, pre);  // past the end: zeros into a tile nobody reads
+    stg.template store_lds<S>(ch.tr != 0, pre);  // past the end: zeros into a tile nobody reads
     stg.store(P, dxc + (size_t)n0 * img, ng, e);
     __syncthreads();  // x of the next group is in the tile
   }
@@ -844,7 +905,7 @@ __global__ __launch_bounds__(kThreads) void strip_bwd(Params P, const T* __restr
   ch.Hs = ch.tr ? P.W : P.H;
   ch.Ws = ch.tr ? P.H : P.W;
   stg.init_lds(P, S, ch.tr != 0, lds_addr(tiles), lds_addr(smem + P.trash));
-  stg.store_lds(P, S, ch.tr != 0, pre);
+  stg.template store_lds<S>(ch.tr != 0, pre);
   __syncthreads();  // x of the first group is in the tile
   float acc[KB];
 #pragma unroll
