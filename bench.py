@@ -25,6 +25,7 @@ over the time at theta = 0 for K in {7, 15, 31, 63}.
 from __future__ import annotations
 
 import argparse
+import gc
 import hashlib
 import json
 import os
@@ -165,6 +166,41 @@ def run_op(ops, case, b, name):
             raise ValueError(name)
 
 
+def timed_steps(torch, dev, steps, names, launch):
+    """Queues `steps` steps (launch(i, name) for every op name in turn) between two device
+    synchronisations.  Returns (wall ms per step, {name: [event ms per launch]}).
+
+    One event before every op; the event before a step's first op also ends the previous
+    step's last op, and one more event ends the last step.  The events are created and
+    recorded once before the timed region (the runtime creates an event at its first
+    record, which can stall the host for a millisecond while the queue is still short),
+    and the collector stays off while the steps are queued."""
+    stream = torch.cuda.current_stream(dev)
+    ev = [torch.cuda.Event(enable_timing=True) for _ in range(steps * len(names) + 1)]
+    for e in ev:
+        e.record(stream)
+    torch.cuda.synchronize()
+    gc_was_on = gc.isenabled()
+    gc.disable()
+    try:
+        t0 = time.perf_counter()
+        k = 0
+        for i in range(steps):
+            for nm in names:
+                ev[k].record(stream)
+                k += 1
+                launch(i, nm)
+        ev[k].record(stream)
+        torch.cuda.synchronize()
+        t1 = time.perf_counter()
+    finally:
+        if gc_was_on:
+            gc.enable()
+    durs = {nm: [ev[i * len(names) + j].elapsed_time(ev[i * len(names) + j + 1]) for i in range(steps)]
+            for j, nm in enumerate(names)}
+    return (t1 - t0) * 1e3 / steps, durs
+
+
 def time_case(case, names, steps, warmup, nsets, torch, ops, synth):
     """Returns (ms_per_step, {op: [durations ms]}) for the ops `names` run in turn per step."""
     dev = torch.device("cuda:0")
@@ -174,34 +210,10 @@ def time_case(case, names, steps, warmup, nsets, torch, ops, synth):
     for i in range(warmup):
         for nm in names:
             run_op(ops, case, sets[i % nsets], nm)
-    stream = torch.cuda.current_stream(dev)
-    # One event before every op; the event before a step's first op also ends
-    # the previous step's last op, and one more event ends the last step.
-    ev = []
-
-    def mark():
-        e = torch.cuda.Event(enable_timing=True)
-        e.record(stream)
-        ev.append(e)
-
-    torch.cuda.synchronize()
-    t0 = time.perf_counter()
-    for i in range(steps):
-        b = sets[i % nsets]
-        for nm in names:
-            mark()
-            run_op(ops, case, b, nm)
-    mark()
-    torch.cuda.synchronize()
-    t1 = time.perf_counter()
-    durs = {nm: [] for nm in names}
-    for i in range(steps):
-        for j, nm in enumerate(names):
-            k = i * len(names) + j
-            durs[nm].append(ev[k].elapsed_time(ev[k + 1]))
+    ms, durs = timed_steps(torch, dev, steps, names, lambda i, nm: run_op(ops, case, sets[i % nsets], nm))
     del sets
     torch.cuda.empty_cache()
-    return (t1 - t0) * 1e3 / steps, durs
+    return ms, durs
 
 
 def op_stats(case, durs):
@@ -210,7 +222,8 @@ def op_stats(case, durs):
     for nm, v in durs.items():
         mean = statistics.fmean(v)
         out[nm] = {"ms_mean": round(mean, 5), "ms_median": round(statistics.median(v), 5),
-                   "ms_std": round(statistics.pstdev(v), 5), "bytes": ab[nm],
+                   "ms_std": round(statistics.pstdev(v), 5),
+                   "ms_max": round(max(v), 5), "max_at_step": v.index(max(v)), "bytes": ab[nm],
                    "GB/s": round(ab[nm] / (mean * 1e-3) / 1e9, 1),
                    "frac_hbm_peak": round(ab[nm] / (mean * 1e-3) / 1e9 / HBM_PEAK_GBS, 4)}
     return out
@@ -263,28 +276,10 @@ def time_dsc(wl, names, steps, warmup, nsets, torch, ops, synth):
     for i in range(warmup):
         for nm in names:
             run_dsc(ops, sets[i % nsets], nm)
-    stream = torch.cuda.current_stream(dev)
-    ev = []
-
-    def mark():
-        e = torch.cuda.Event(enable_timing=True)
-        e.record(stream)
-        ev.append(e)
-
-    torch.cuda.synchronize()
-    t0 = time.perf_counter()
-    for i in range(steps):
-        for nm in names:
-            mark()
-            run_dsc(ops, sets[i % nsets], nm)
-    mark()
-    torch.cuda.synchronize()
-    t1 = time.perf_counter()
-    durs = {nm: [ev[i * len(names) + j].elapsed_time(ev[i * len(names) + j + 1]) for i in range(steps)]
-            for j, nm in enumerate(names)}
+    ms, durs = timed_steps(torch, dev, steps, names, lambda i, nm: run_dsc(ops, sets[i % nsets], nm))
     del sets
     torch.cuda.empty_cache()
-    return (t1 - t0) * 1e3 / steps, durs
+    return ms, durs
 
 
 def dsc_stats(wl, ms, durs):
