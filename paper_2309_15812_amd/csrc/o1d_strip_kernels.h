@@ -42,6 +42,7 @@
 #include <stdint.h>
 
 #include <atomic>
+#include <type_traits>
 #include <utility>
 
 #include "o1d_device.h"
@@ -919,17 +920,6 @@ __global__ __launch_bounds__(kThreads) void strip_bwd(Params P, const T* __restr
   write_partial<KB>(P, pg, smem + P.trash - kWaves * 64, ch.ncells, acc, partial);
 }
 
-// dw[i] = sum over the partial rows, in a fixed order.
-template <typename T>
-__global__ __launch_bounds__(256) void strip_wgrad_reduce(const float* __restrict__ partial, T* __restrict__ dw,
-                                                          int CK, int parts) {
-  const int i = blockIdx.x * blockDim.x + threadIdx.x;
-  if (i >= CK) return;
-  float s = 0.f;
-  for (int j = 0; j < parts; ++j) s += partial[(size_t)j * CK + i];
-  dw[i] = from_f32<T>(s);
-}
-
 // ---------------------------------------------------------------- launch
 
 // Fits the grid to `per_cu` resident workgroups on every CU of the device.
@@ -1029,10 +1019,8 @@ hipError_t wgrad_t(const Plan& pl, const void* x, const void* dy, const float* t
   O1D_STRIP_STRIDES(O1D_CASE)
 #undef O1D_CASE
   if (e != hipSuccess) return e;
-  const int CK = pl.p.C * pl.p.K;
-  hipLaunchKernelGGL(strip_wgrad_reduce<T>, dim3((unsigned)((CK + 255) / 256)), dim3(256), 0, stream, partial,
-                     static_cast<T*>(dw), CK, pl.blocks_n);
-  return hipGetLastError();
+  return launch_partial_sum(std::is_same<T, float>::value ? Dtype::F32 : Dtype::BF16, partial, dw, pl.p.C * pl.p.K,
+                            pl.blocks_n, stream);
 }
 
 template <typename T, int S, int KB>
@@ -1055,10 +1043,8 @@ hipError_t bwd_t(const Plan& pl, const void* x, const void* dy, const void* w, c
   O1D_STRIP_STRIDES(O1D_CASE)
 #undef O1D_CASE
   if (e != hipSuccess) return e;
-  const int CK = pl.p.C * pl.p.K;
-  hipLaunchKernelGGL(strip_wgrad_reduce<T>, dim3((unsigned)((CK + 255) / 256)), dim3(256), 0, stream, partial,
-                     static_cast<T*>(dw), CK, pl.blocks_n);
-  return hipGetLastError();
+  return launch_partial_sum(std::is_same<T, float>::value ? Dtype::F32 : Dtype::BF16, partial, dw, pl.p.C * pl.p.K,
+                            pl.blocks_n, stream);
 }
 
 template <typename T, int KB>
