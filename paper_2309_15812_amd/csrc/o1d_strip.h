@@ -175,9 +175,9 @@ inline Plan plan_strip(int N, int C, int H, int W, int K, int sign, int kind, bo
   p.mc = mc;
   p.TR = cover + 2 * halo;
   // the last row's right-hand reads run up to mc + M + mc - S columns past
-  // the tile
+  // the tile; slots are a whole number of 16-byte chunks
   const int tail = mc + M + mc - S > kGuard ? mc + M + mc - S : kGuard;
-  p.PS = p.TR * S + kGuard + tail;
+  p.PS = (p.TR * S + kGuard + tail + 3) & ~3;
   p.ks = cdiv(H, 8 * kWaves);
   p.ms = cdiv(W, 32);
   const int per_plane_slots = p.ks * p.ms;

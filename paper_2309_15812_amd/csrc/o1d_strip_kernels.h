@@ -78,23 +78,32 @@ struct Prog {
 };
 static_assert(sizeof(Prog) == kProgWords * 4, "kProgWords must match the program layout");
 
-__device__ __forceinline__ int wave_min_i(int v) {
-#pragma unroll
-  for (int m = 32; m >= 1; m >>= 1) v = min(v, __shfl_xor(v, m, 64));
-  return v;
+// OR over the 64 lanes of a wave, returned uniform: an inclusive scan with
+// DPP row shifts (1, 2, 4, 8 within rows of 16 lanes), then row broadcasts
+// of lanes 15 and 31 into the rows above; lane 63 holds the total.  Lanes
+// whose DPP source is outside the row or row mask contribute 0.  All 64
+// lanes must be active.
+template <class F>
+__device__ __forceinline__ uint32_t wave_reduce_dpp(uint32_t v, F op) {
+  v = op(v, (uint32_t)__builtin_amdgcn_update_dpp(0, (int)v, 0x111, 0xf, 0xf, false));  // row_shr:1
+  v = op(v, (uint32_t)__builtin_amdgcn_update_dpp(0, (int)v, 0x112, 0xf, 0xf, false));  // row_shr:2
+  v = op(v, (uint32_t)__builtin_amdgcn_update_dpp(0, (int)v, 0x114, 0xf, 0xf, false));  // row_shr:4
+  v = op(v, (uint32_t)__builtin_amdgcn_update_dpp(0, (int)v, 0x118, 0xf, 0xf, false));  // row_shr:8
+  v = op(v, (uint32_t)__builtin_amdgcn_update_dpp(0, (int)v, 0x142, 0xa, 0xf, false));  // row_bcast:15
+  v = op(v, (uint32_t)__builtin_amdgcn_update_dpp(0, (int)v, 0x143, 0xc, 0xf, false));  // row_bcast:31
+  return (uint32_t)__builtin_amdgcn_readlane((int)v, 63);
 }
-__device__ __forceinline__ int wave_max_i(int v) {
-#pragma unroll
-  for (int m = 32; m >= 1; m >>= 1) v = max(v, __shfl_xor(v, m, 64));
-  return v;
+__device__ __forceinline__ uint32_t wave_or32(uint32_t v) {
+  return wave_reduce_dpp(v, [](uint32_t x, uint32_t y) { return x | y; });
+}
+// Sum over the 64 lanes (0 is the bit pattern of +0.0f), in a fixed order.
+__device__ __forceinline__ float wave_sum(float v) {
+  return __uint_as_float(wave_reduce_dpp(__float_as_uint(v), [](uint32_t x, uint32_t y) {
+    return __float_as_uint(__uint_as_float(x) + __uint_as_float(y));
+  }));
 }
 __device__ __forceinline__ uint64_t wave_or(uint64_t m) {
-#pragma unroll
-  for (int i = 32; i >= 1; i >>= 1) {
-    const uint32_t lo = __shfl_xor((uint32_t)m, i, 64), hi = __shfl_xor((uint32_t)(m >> 32), i, 64);
-    m |= ((uint64_t)hi << 32) | lo;
-  }
-  return m;
+  return ((uint64_t)wave_or32((uint32_t)(m >> 32)) << 32) | wave_or32((uint32_t)m);
 }
 __device__ __forceinline__ uint64_t below_mask(int n) { return n <= 0 ? 0ull : (n >= 64 ? ~0ull : (~0ull >> (64 - n))); }
 __device__ __forceinline__ uint64_t above_mask(int n) { return n >= 63 ? 0ull : (~0ull << (n + 1)); }
@@ -122,8 +131,11 @@ __device__ void build_prog(Prog* pg, const T* __restrict__ wgt, float theta, int
     dw *= sign;
     if (wgt) wk = to_f32(wgt[(size_t)c * K + k]);
   }
-  const int hmin = wave_min_i(act ? dh : 1 << 20), hmax = wave_max_i(act ? dh : -(1 << 20));
-  const int wmin = wave_min_i(act ? dw : 1 << 20), wmax = wave_max_i(act ? dw : -(1 << 20));
+  // The offsets of Eq. (2) are monotone in k (a floor of a linear function
+  // of k, clamped), so their extremes are those of the first and last taps.
+  const int h0 = __builtin_amdgcn_readlane(dh, 0), h1 = __builtin_amdgcn_readlane(dh, K - 1);
+  const int w0 = __builtin_amdgcn_readlane(dw, 0), w1 = __builtin_amdgcn_readlane(dw, K - 1);
+  const int hmin = min(h0, h1), hmax = max(h0, h1), wmin = min(w0, w1), wmax = max(w0, w1);
   const bool tr = (wmax - wmin) > (hmax - hmin);
   const int a = tr ? dw : dh;  // row offset in the staging frame
   const int b = tr ? dh : dw;  // column offset in the staging frame
@@ -148,7 +160,8 @@ __device__ void build_prog(Prog* pg, const T* __restrict__ wgt, float theta, int
 
   // cell order: frame rows increasing
   const int lfirst = lobit(cellm), llast = hibit(cellm);
-  const int a_first = __shfl(a, lfirst > 63 ? 0 : lfirst, 64), a_last = __shfl(a, llast < 0 ? 0 : llast, 64);
+  const int a_first = __builtin_amdgcn_readlane(a, lfirst > 63 ? 0 : lfirst),
+            a_last = __builtin_amdgcn_readlane(a, llast < 0 ? 0 : llast);
   const bool rev = a_last < a_first;
   const int co = rev ? ncells - 1 - ci : ci;
   const int pc = rev ? lobit(cellm & above_mask(k)) : hibit(cellm & below_mask(k));  // predecessor cell lane
@@ -187,6 +200,14 @@ __device__ void build_prog(Prog* pg, const T* __restrict__ wgt, float theta, int
     pg->s = s;
     pg->finite = allfin ? 1 : 0;
   }
+}
+
+// Zeroes the group's tile slots with 16-byte stores (slots are a multiple
+// of 4 words and start 16-byte aligned).
+__device__ __forceinline__ void zero_tiles(const Params& P, float* tiles) {
+  float4* t4 = reinterpret_cast<float4*>(tiles);
+  const int n4 = (P.G * P.PS) >> 2;
+  for (int i = threadIdx.x; i < n4; i += kThreads) t4[i] = make_float4(0.f, 0.f, 0.f, 0.f);
 }
 
 // ---------------------------------------------------------------- walk
@@ -664,7 +685,7 @@ __global__ __launch_bounds__(kThreads) void strip_gather(Params P, const T* __re
   stg.init_global(P);
   uint32_t pre[Stage<T>::kWords];
   stg.load(P, inc + (size_t)n_begin * img, min(P.G, n_end - n_begin), pre);
-  for (int i = tid; i < P.G * P.PS; i += kThreads) tiles[i] = 0.f;  // margins and guards stay zero
+  zero_tiles(P, tiles);  // margins and guards stay zero
   if (wave == 0) build_prog<T>(pg, wgt, theta[c], c, P.K, P.sign, P.H, P.W, S);
   __syncthreads();
   Chan ch;
@@ -741,9 +762,7 @@ __device__ __forceinline__ void write_partial(const Params& P, const Prog* pg, f
 #pragma unroll
   for (int ci = 0; ci < KB; ++ci) {
     if (ci < ncells) {
-      float v = acc[ci];
-#pragma unroll
-      for (int m = 32; m >= 1; m >>= 1) v += __shfl_xor(v, m, 64);
+      const float v = wave_sum(acc[ci]);
       if (lane == 0) red[wave * 64 + ci] = v;
     }
   }
@@ -780,7 +799,7 @@ __global__ __launch_bounds__(kThreads, 2) void strip_wgrad(Params P, const T* __
   stg.init_global(P);
   uint32_t xpre[Stage<T>::kWords];
   stg.load(P, xc + (size_t)n_begin * img, min(P.G, n_end - n_begin), xpre);
-  for (int i = tid; i < P.G * P.PS; i += kThreads) tiles[i] = 0.f;  // margins and guards stay zero
+  zero_tiles(P, tiles);  // margins and guards stay zero
   if (wave == 0) build_prog<T>(pg, static_cast<const T*>(nullptr), theta[c], c, P.K, 1, P.H, P.W, S);
   __syncthreads();
   Chan ch;
@@ -891,7 +910,7 @@ __global__ __launch_bounds__(kThreads) void strip_bwd(Params P, const T* __restr
   stg.init_global(P);
   uint32_t pre[Stage<T>::kWords];
   stg.load(P, xc + (size_t)n_begin * img, min(P.G, n_end - n_begin), pre);
-  for (int i = tid; i < P.G * P.PS; i += kThreads) tiles[i] = 0.f;  // margins and guards stay zero
+  zero_tiles(P, tiles);  // margins and guards stay zero
   if (wave == 0) build_prog<T>(pg, wgt, theta[c], c, P.K, -1, P.H, P.W, S);
   __syncthreads();
   Chan ch;
