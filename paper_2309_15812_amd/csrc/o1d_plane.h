@@ -13,7 +13,9 @@
 // consecutive words), with a margin of only (RP - 1) rows and
 // (R - 1) columns (times the stride, plus one for bilinear corners): cells
 // that fall outside the plane for a whole group of RP x R outputs are not
-// visited at all, instead of reading zeros from a margin of K / 2.
+// visited at all, instead of reading zeros from a margin of K / 2.  The
+// column margin is one gap per row, shared by a row's right-hand and the
+// next row's left-hand reads.
 #pragma once
 
 #include <stddef.h>
@@ -45,7 +47,8 @@ struct Params {
   int NI, lni, R;   // lanes: NI / 2 image pairs (NI a power of two, lni its log2) x R output columns
   int RP;           // output rows per lane
   int mr, mc;       // tile margins (rows, columns)
-  int TRm, TCm;     // tile rows and columns: H + 2 mr, W + 2 mc
+  int TRm, TCm;     // tile rows H + 2 mr; tile row stride W + mc (consecutive rows share one gap of mc
+                    // zero columns as their right and left margins; mc more columns end the tile)
   int nrg, ncg;     // row groups (of RP rows) and column groups (of R columns) of the output plane
   int nitems;       // nrg ncg
   int OSz;          // elements per image of the output-shaped tile (an odd number of 32-bit words)
@@ -117,7 +120,7 @@ inline Plan plan_plane(int op, int N, int C, int H, int W, int K, int str, int m
       p.mr = (RP - 1) * p.sig + mode;
       p.mc = (p.R - 1) * p.sig + mode;
       p.TRm = H + 2 * p.mr;
-      p.TCm = W + 2 * p.mc;
+      p.TCm = W + p.mc;
       p.nrg = cdiv(p.OH, RP);
       p.ncg = cdiv(p.OW, p.R);
       p.nitems = p.nrg * p.ncg;
@@ -133,7 +136,8 @@ inline Plan plan_plane(int op, int N, int C, int H, int W, int K, int str, int m
       p.ival_off = (int)align16((size_t)p.ncap * 24 + (size_t)(2 * K + 1) * 4);  // cells (offset and weight,
       // row and column, tap, coefficient), first cell per tap, per-tap counts
       p.table_bytes = (int)align16((size_t)p.ival_off + (size_t)(p.nrg + p.ncg) * 8);  // then the runs
-      size_t rest = align16((size_t)p.TRm * p.TCm * NI * 4) + align16((size_t)NI * p.OSz * esize);
+      const size_t tile = align16(((size_t)p.TRm * p.TCm + p.mc) * NI * 4);
+      size_t rest = tile + align16((size_t)NI * p.OSz * esize);
       if (reduce) rest += align16((size_t)(kWaves * p.KB + K) * 4);
       p.nchunk = cdiv(N, NI);
       const long long nitem = (long long)C * p.nchunk;
@@ -144,18 +148,28 @@ inline Plan plan_plane(int op, int N, int C, int H, int W, int K, int str, int m
       const size_t off = (size_t)p.table_bytes + rest;
       if (off > kLdsBudget) continue;
       p.tile_off = p.nslot * p.table_bytes;
-      p.aux_off = p.tile_off + (int)align16((size_t)p.TRm * p.TCm * NI * 4);
+      p.aux_off = p.tile_off + (int)tile;
       p.red_off = p.aux_off + (int)align16((size_t)NI * p.OSz * esize);
       const long long blocks = (nitem + p.per - 1) / p.per;
       p.nblocks = (int)blocks;
       // idle lanes (images past N, rows and columns past the plane), one
       // table read per cell and RP tile reads, the cells a group's run adds
       // for its extent (R - 1 columns, RP - 1 rows), too few workgroups for
-      // 256 CUs, a single workgroup per CU
+      // 256 CUs, a single workgroup per CU, and the idle share of the last
+      // round of workgroups (resident per CU by LDS, granted in 1 KB steps,
+      // at most four of eight waves)
       double score = (double)p.nchunk * NI / N * ((double)p.nrg * RP / p.OH) * ((double)p.ncg * p.R / p.OW) *
                      (1.0 + 0.5 / RP) * (1.0 + (double)(p.R - 1) / p.OW) * (1.0 + (double)(RP - 1) / p.OH);
       if (blocks < 640) score *= 640.0 / (double)blocks;
       if (kMaxLdsBytes / off < 2) score *= 1.5;
+      {
+        const size_t granted = (off + 1023) / 1024 * 1024;
+        long long resident = (long long)((kMaxLdsBytes - 512) / granted);
+        if (resident > 4) resident = 4;
+        if (resident < 1) resident = 1;
+        const long long slots = 256 * resident, rounds = (blocks + slots - 1) / slots;
+        score *= (double)(rounds * slots) / (double)blocks;
+      }
       if (!best.ok || score < best_score - 1e-9) {
         best_score = score;
         best.p = p;

@@ -141,7 +141,7 @@ __device__ void build_cells(const Params& P, const Lds& L, float th, float wk) {
 // plane).  The barriers of build_cells order it before staging.
 __device__ __forceinline__ void prepare(const Params& P, const Lds& L) {
   float4* t4 = reinterpret_cast<float4*>(L.tile);
-  const int n4 = P.TRm * P.TCm * P.NI / 4;
+  const int n4 = (P.TRm * P.TCm + P.mc) * P.NI / 4;
   for (int i = threadIdx.x; i < n4; i += kThreads) t4[i] = make_float4(0.f, 0.f, 0.f, 0.f);
 }
 
