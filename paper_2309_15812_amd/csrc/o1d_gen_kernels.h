@@ -182,34 +182,50 @@ __device__ __forceinline__ int fdiv(int a, int b, float rb) {
 // of ng images between global memory and LDS: for every element (g, i, j,
 // ch), with j (NCHW) or ch (NHWC) fastest so that neighbouring lanes touch
 // neighbouring addresses, op.load(g, i, j, ch) gives the value and
-// op.store(g, i, j, ch, v) puts it.  Eight elements per lane are loaded
-// before any is stored, so that their memory latencies overlap.
+// op.store(g, i, j, ch, v) puts it.  A lane keeps one position x in the
+// row (rows shorter than the workgroup: rpp rows per pass; longer rows:
+// chunks of kThreads) and steps through its rows with an incremental (g, i),
+// so the index arithmetic is per lane, not per element.  Eight rows per lane
+// are loaded before any is stored, so that their memory latencies overlap.
 template <int L, class Op>
 __device__ __forceinline__ void copy_rect(int ng, int ni, int nj, int lcb, Op&& op) {
   const int inner = nj << (L == kNHWC ? lcb : 0);
-  const int per = ni * inner, total = ng * per;
-  if (total <= 0) return;
-  const float rper = 1.f / (float)per, rinner = 1.f / (float)inner;
-  for (int e0 = 0; e0 < total; e0 += 8 * kThreads) {
-    float v[8];
-    int gg[8], ii[8], jj[8], cc[8];
+  const int rows = ng * ni;
+  if (rows <= 0 || inner <= 0) return;
+  const int t = threadIdx.x;
+  const bool wide = inner >= kThreads;
+  const int rpp = wide ? 1 : kThreads / inner;  // rows per pass
+  const int ro = wide ? 0 : t / inner;           // the lane's first row
+  if (ro >= rpp) return;                         // lanes past rpp rows of a pass
+  const int rdiv = rpp / ni, rmod = rpp - rdiv * ni;
+  const int g0 = ro / ni, i0 = ro - g0 * ni;
+  for (int x = wide ? t : t - ro * inner; x < inner; x += kThreads) {
+    const int j = L == kNHWC ? x >> lcb : x;
+    const int ch = L == kNHWC ? x & ((1 << lcb) - 1) : 0;
+    int g = g0, i = i0;
+    for (int row = ro; row < rows;) {
+      float v[8];
+      int gg[8], ii[8];
 #pragma unroll
-    for (int m = 0; m < 8; ++m) {
-      const int e = e0 + threadIdx.x + kThreads * m;
-      gg[m] = -1;
-      if (e < total) {
-        const int g = fdiv(e, per, rper), r = e - g * per;
-        const int i = fdiv(r, inner, rinner), x = r - i * inner;
-        gg[m] = g;
-        ii[m] = i;
-        jj[m] = L == kNHWC ? x >> lcb : x;
-        cc[m] = L == kNHWC ? x & ((1 << lcb) - 1) : 0;
-        v[m] = op.load(g, i, jj[m], cc[m]);
+      for (int m = 0; m < 8; ++m) {
+        gg[m] = -1;
+        if (row < rows) {
+          gg[m] = g;
+          ii[m] = i;
+          v[m] = op.load(g, i, j, ch);
+        }
+        row += rpp;
+        g += rdiv;
+        i += rmod;
+        if (i >= ni) {
+          i -= ni;
+          ++g;
+        }
       }
-    }
 #pragma unroll
-    for (int m = 0; m < 8; ++m)
-      if (gg[m] >= 0) op.store(gg[m], ii[m], jj[m], cc[m], v[m]);
+      for (int m = 0; m < 8; ++m)
+        if (gg[m] >= 0) op.store(gg[m], ii[m], j, ch, v[m]);
+    }
   }
 }
 
@@ -349,17 +365,34 @@ __global__ __launch_bounds__(kThreads) void gen_gather(Params P, const T* __rest
     const int ng = min(P.G, wk.n_end - n0);
     stage<T, L>(P, wk, in, tiles, n0, ng);
     __syncthreads();
-    for (int ch = 0; ch < P.CB; ++ch) {
-      // one channel at a time: its cell count and table are uniform
-      const int nc = __builtin_amdgcn_readfirstlane(cl.cnt[ch]);
-      const int4* cw2 = reinterpret_cast<const int4*>(cl.cw + 2 * ch * cl.ncap);
-      for (int tau = threadIdx.x; tau < ng * per_ch; tau += kThreads) {
+    // NCHW (one channel per block): its cell count and table are uniform.
+    // NHWC: the block's CB channels share one pass (a channel alone would
+    // leave most lanes idle on a narrow band); every lane reads its own
+    // channel's table, and the walk runs to the block's largest cell count
+    // (tables are zero past their cells: offset 0, weight 0).
+    const int npass = L == kNHWC ? 1 : P.CB;
+    for (int ch = 0; ch < npass; ++ch) {
+      int nc = 0;
+      if (L == kNHWC) {
+        for (int c = 0; c < P.CB; ++c) nc = max(nc, __builtin_amdgcn_readfirstlane(cl.cnt[c]));
+      } else {
+        nc = __builtin_amdgcn_readfirstlane(cl.cnt[ch]);
+      }
+      const int ntask = ng * per_ch * (L == kNHWC ? P.CB : 1);
+      for (int tau = threadIdx.x; tau < ntask; tau += kThreads) {
         Task t;
         t.qq = tau % P.BQ;
-        const int r = tau / P.BQ;
+        int r = tau / P.BQ;
         t.rg = r % P.NRG;
-        t.g = r / P.NRG;
-        t.ch = ch;
+        r /= P.NRG;
+        if (L == kNHWC) {
+          t.ch = r & (P.CB - 1);
+          t.g = r >> P.lcb;
+        } else {
+          t.ch = ch;
+          t.g = r;
+        }
+        const int4* cw2 = reinterpret_cast<const int4*>(cl.cw + 2 * t.ch * cl.ncap);
         const float* tl = tile_of(P, tiles, t);
         float acc[RP];
 #pragma unroll
@@ -408,7 +441,7 @@ __global__ __launch_bounds__(kThreads) void gen_gather(Params P, const T* __rest
             }
           }
         } else {
-          float* b = band + (t.g * P.CB + ch) * P.OS + t.rg * RP * P.BQ + t.qq;
+          float* b = band + (t.g * P.CB + t.ch) * P.OS + t.rg * RP * P.BQ + t.qq;
 #pragma unroll
           for (int i = 0; i < RP; ++i) b[i * P.BQ] = acc[i];
         }
