@@ -478,6 +478,27 @@ __device__ __forceinline__ void fold_cells(const Params& P, const Cells& cl, flo
   __syncthreads();
 }
 
+// fold_cells for cpp channels c0 .. c0 + cpp - 1 at once, channel c0 + i
+// held by waves i wpc .. i wpc + wpc - 1: each channel's wave sums are
+// added in a fixed order by its own thread.
+template <int KB>
+__device__ __forceinline__ void fold_group(const Params& P, const Cells& cl, float (&acc)[KB], int c0, int cpp,
+                                           int wpc, int j0, float* red, float* dwacc) {
+  wave::sums<KB>(acc, red);
+  __syncthreads();
+  if ((int)threadIdx.x < cpp) {
+    const int ch = c0 + threadIdx.x;
+    const int nc = cl.cnt[ch];
+    for (int j = 0; j < KB && j0 + j < nc; ++j) {
+      float v = 0.f;
+      for (int w = threadIdx.x * wpc; w < (int)(threadIdx.x + 1) * wpc; ++w) v += red[w * KB + j];
+      const int cj = ch * cl.ncap + j0 + j;
+      dwacc[ch * P.K + cl.tap[cj]] += cl.coef[cj] * v;
+    }
+  }
+  __syncthreads();
+}
+
 // acc[j] += sum_i d[i] tile[base + off_j + i rstep] for the cells of the
 // group of KB: eight cells per step (one branch per step, the 8 RP reads
 // issued together), steps past nc skipped (nc uniform; cells between the
@@ -537,6 +558,15 @@ __global__ __launch_bounds__(kThreads) void gen_wgrad(Params P, const T* __restr
   __syncthreads();
   const int rstep = P.sig * P.TC;
   const int per_ch = P.NRG * P.BQ;  // tasks per image and channel
+  // A lane keeps one channel: a pass covers cpp channels with wpc whole
+  // waves each (NCHW: one channel, all waves), so that every wave's cell
+  // count is uniform and its per-cell sums belong to one channel.
+  constexpr int nw = kThreads / 64;
+  const int cpp = L == kNCHW ? 1 : min(P.CB, nw), wpc = nw / cpp, npass = L == kNCHW ? 1 : P.CB / cpp;
+  const int wave = __builtin_amdgcn_readfirstlane(threadIdx.x >> 6);
+  // the lane's first task in its channel and its task step
+  const int lt = L == kNCHW ? (int)threadIdx.x : (wave % wpc) * 64 + (threadIdx.x & 63);
+  const int lstep = L == kNCHW ? kThreads : wpc * 64;
   for (int j0 = 0; j0 < P.nck * KB; j0 += KB) {
     float acc[KB];
 #pragma unroll
@@ -546,11 +576,12 @@ __global__ __launch_bounds__(kThreads) void gen_wgrad(Params P, const T* __restr
       stage<T, L>(P, wk, x, tiles, n0, ng);
       stage_band<T, L>(P, wk, dy, band, n0, ng);
       __syncthreads();
-      for (int ch = 0; ch < P.CB; ++ch) {
-        const int nc = min(KB, __builtin_amdgcn_readfirstlane(cl.cnt[ch]) - j0);  // uniform
+      for (int ps = 0; ps < npass; ++ps) {
+        const int ch = L == kNCHW ? 0 : ps * cpp + wave / wpc;                   // uniform per wave
+        const int nc = min(KB, __builtin_amdgcn_readfirstlane(cl.cnt[ch]) - j0);  // uniform per wave
         if (nc > 0) {
           const int2* cw = reinterpret_cast<const int2*>(cl.cw) + ch * cl.ncap + j0;
-          for (int tau = threadIdx.x; tau < ng * per_ch; tau += kThreads) {
+          for (int tau = lt; tau < ng * per_ch; tau += lstep) {
             Task t;
             t.qq = tau % P.BQ;
             const int r = tau / P.BQ;
@@ -564,15 +595,20 @@ __global__ __launch_bounds__(kThreads) void gen_wgrad(Params P, const T* __restr
             cell_dots<RP, KB>(cw, nc, tile_of(P, tiles, t), rstep, d, acc);
           }
         }
-        if (L == kNHWC) {
-          if (nc > 0) fold_cells<KB>(P, cl, acc, ch, j0, red, dwacc);
+        if (npass > 1) {
+          // the next pass takes other channels: fold these
+          fold_group<KB>(P, cl, acc, ps * cpp, cpp, wpc, j0, red, dwacc);
 #pragma unroll
           for (int j = 0; j < KB; ++j) acc[j] = 0.f;
         }
       }
       __syncthreads();  // the tiles are free
     }
-    if (L == kNCHW && j0 < __builtin_amdgcn_readfirstlane(cl.cnt[0])) fold_cells<KB>(P, cl, acc, 0, j0, red, dwacc);
+    if (L == kNCHW) {
+      if (j0 < __builtin_amdgcn_readfirstlane(cl.cnt[0])) fold_cells<KB>(P, cl, acc, 0, j0, red, dwacc);
+    } else if (npass == 1) {
+      fold_group<KB>(P, cl, acc, 0, cpp, wpc, j0, red, dwacc);
+    }
   }
   for (int i = threadIdx.x; i < P.CB * P.K; i += kThreads) {
     const int ch = i / P.K, k = i - ch * P.K, c = wk.c0 + ch;
