@@ -78,6 +78,9 @@ def parse():
     ap.add_argument("--no-cpu", action="store_true", help="skip the CPU oracle baseline")
     ap.add_argument("--no-extra", action="store_true", help="only the headline step (no configs, sweep, copy)")
     ap.add_argument("--cpu-seconds", type=float, default=12.0, help="target CPU work for the oracle sample")
+    ap.add_argument("--case", default="", help="profiling aid, with --only: run that op on one of the configs "
+                    "of the bench line (nhwc_stage1, nhwc_stage3_bf16, stride2_224, bilinear_stage1, ...) "
+                    "instead of the headline workload")
     ap.add_argument("--only", default="", help="profiling aid: run only this op (fwd|bwd|bwd_input|bwd_weight), or "
                     "'copy': a plain elementwise copy of one N*C*H*W tensor (reads T bytes, writes T bytes), "
                     "the calibration kernel for the HBM byte counters, or dsc_fwd|dsc_bwd: the depthwise "
@@ -199,6 +202,21 @@ def timed_steps(torch, dev, steps, names, launch):
     durs = {nm: [ev[i * len(names) + j].elapsed_time(ev[i * len(names) + j + 1]) for i in range(steps)]
             for j, nm in enumerate(names)}
     return (t1 - t0) * 1e3 / steps, durs
+
+
+def config_cases(synth):
+    """The other workloads of the bench line: {name: (Case, ops timed)}."""
+    W = synth.WORKLOADS
+    return {
+        "c2_stage1_fwd": (Case(W["c2"]), ["fwd"]),
+        "c3_stage2": (Case(W["c3"]), ["fwd", "bwd"]),
+        "c4_stage3_bf16": (Case(W["c4"]), ["fwd", "bwd"]),
+        "nhwc_stage1": (Case(W["metric"], layout="nhwc"), ["fwd", "bwd_input", "bwd_weight"]),
+        "nhwc_stage3_bf16": (Case(W["c4"], layout="nhwc"), ["fwd", "bwd_input", "bwd_weight"]),
+        "stride2_224": (Case(W["metric"].replace(name="s2", N=8, H=224, W=224), stride=2),
+                        ["fwd", "bwd_input", "bwd_weight"]),
+        "bilinear_stage1": (Case(W["metric"], sampling="bilinear"), ["fwd", "bwd_input", "bwd_weight"]),
+    }
 
 
 def time_case(case, names, steps, warmup, nsets, torch, ops, synth):
@@ -393,6 +411,11 @@ def main():
         return
     wl = synth.WORKLOADS[args.workload]
     head = Case(wl)
+    if args.case:
+        if not args.only:
+            sys.exit("--case needs --only")
+        head = config_cases(synth)[args.case][0]
+        wl = head.wl
     T = wl.elems * wl.elem_bytes
     print(f"[bench] workload {wl} T={T / 1e6:.2f} MB sets={args.sets}", file=sys.stderr, flush=True)
     names = [args.only] if args.only else ["fwd", "bwd"]
@@ -434,7 +457,8 @@ def main():
             "peak": HBM_PEAK_GBS,
             "unit": "GB/s",
             "frac": round(achieved / HBM_PEAK_GBS, 4),
-            "traffic": traffic_for(dominant),
+            # the committed counter summary covers the headline workload only
+            "traffic": traffic_for(dominant) if args.workload == "metric" and not args.case else None,
             "algorithmic_bytes_per_launch": op_bytes[dominant],
             "ms_per_launch": dom_ms,
         },
@@ -450,16 +474,7 @@ def main():
         print(f"[bench] copy: {out['copy']}", file=sys.stderr, flush=True)
         # the other workloads, per op
         W = synth.WORKLOADS
-        cases = {
-            "c2_stage1_fwd": (Case(W["c2"]), ["fwd"]),
-            "c3_stage2": (Case(W["c3"]), ["fwd", "bwd"]),
-            "c4_stage3_bf16": (Case(W["c4"]), ["fwd", "bwd"]),
-            "nhwc_stage1": (Case(W["metric"], layout="nhwc"), ["fwd", "bwd_input", "bwd_weight"]),
-            "nhwc_stage3_bf16": (Case(W["c4"], layout="nhwc"), ["fwd", "bwd_input", "bwd_weight"]),
-            "stride2_224": (Case(W["metric"].replace(name="s2", N=8, H=224, W=224), stride=2),
-                            ["fwd", "bwd_input", "bwd_weight"]),
-            "bilinear_stage1": (Case(W["metric"], sampling="bilinear"), ["fwd", "bwd_input", "bwd_weight"]),
-        }
+        cases = config_cases(synth)
         cfg = {}
         for key, (case, nm) in cases.items():
             m, dd = time_case(case, nm, 20, 5, 3, torch, ops, synth)
