@@ -316,21 +316,21 @@ struct PlaneLoad {
   }
 };
 
-// Builds the cell tables (and their runs) of channels c0 .. c1 into slots
-// 0 .. c1 - c0 (one slot per workgroup here: c1 = c0), all inputs of each
-// build loaded before it starts; leaves slot 0 in use.  Barriers inside; the caller orders the runs before their use
-// with a barrier.
+// Thread k's tap weight of channel c (0 past the taps, or without weights).
+// Loaded before the plane's loads, so that the cell tables wait for this
+// load only: vector loads complete in order.
 template <typename T>
-__device__ __forceinline__ void tables(const Params& P, Lds& L, const T* __restrict__ wgt,
-                                       const float* __restrict__ theta, int c0, int c1) {
-  for (int c = c0; c <= c1; ++c) {
-    const float th = theta[c];
-    const float wk = wgt && (int)threadIdx.x < P.K ? to_f32(wgt[(size_t)c * P.K + threadIdx.x]) : 0.f;
-    L.use(P, c - c0);
-    build_cells(P, L, th, wk);
-    cell_runs(P, L);
-  }
+__device__ __forceinline__ float tap_weight(const Params& P, const T* __restrict__ wgt, int c) {
+  return wgt && (int)threadIdx.x < P.K ? to_f32(wgt[(size_t)c * P.K + threadIdx.x]) : 0.f;
+}
+
+// The cell tables (and their runs) of one channel from its angle th and
+// thread k's tap weight wk, into slot 0.  Barriers inside; the caller orders
+// the runs before their use.
+__device__ __forceinline__ void tables(const Params& P, Lds& L, float th, float wk) {
   L.use(P, 0);
+  build_cells(P, L, th, wk);
+  cell_runs(P, L);
 }
 
 // The output-shaped tile's images of item `it` to channel c of dst.
@@ -458,10 +458,12 @@ __device__ __forceinline__ void gather_one(const Params& P, Lds& L, const T* __r
   const Share sh(P);
   const Item it(P, blockIdx.x);
   T* aux = reinterpret_cast<T*>(L.aux);
+  const float th = theta[it.c];
+  const float wk = tap_weight<T>(P, wgt, it.c);
   PlaneLoad<T, V> pl;
   pl.issue(P, sh, in, it, P.SH * P.SW);
   prepare(P, L);
-  tables(P, L, wgt, theta, it.c, it.c);
+  tables(P, L, th, wk);
   pl.commit_tile(P, sh, L.tile);
   __syncthreads();
   gather_item<T, RP>(P, L, aux);
@@ -602,7 +604,7 @@ __global__ __launch_bounds__(kThreads) void plane_wgrad(Params P, const T* __res
   prepare(P, L);
   {
     const Item it(P, blockIdx.x);
-    tables(P, L, static_cast<const T*>(nullptr), theta, it.c, it.c);
+    tables(P, L, theta[it.c], 0.f);
     if (P.vt == 4) {
       PlaneLoad<T, 4> pl;
       pl.issue(P, sh, x, it, P.SH * P.SW);
@@ -689,11 +691,13 @@ __device__ __forceinline__ void bwd_one(const Params& P, Lds& L, const T* __rest
   T* aux = reinterpret_cast<T*>(L.aux);
   float* dwacc = L.red + kWaves * KB;
   for (int k = threadIdx.x; k < P.K; k += kThreads) dwacc[k] = 0.f;
+  const float th = theta[it.c];
+  const float wk = tap_weight<T>(P, wgt, it.c);
   PlaneLoad<T, V> pd, px;
   pd.issue(P, sh, dy, it, E);
   px.issue(P, sh, x, it, E);
   prepare(P, L);
-  tables(P, L, wgt, theta, it.c, it.c);
+  tables(P, L, th, wk);
   pd.commit_tile(P, sh, L.tile);
   px.commit_aux(P, sh, aux);
   __syncthreads();
