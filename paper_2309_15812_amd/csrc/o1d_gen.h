@@ -25,7 +25,14 @@ namespace gen {
 constexpr int kThreads = 256;
 constexpr int kMaxK = 127;
 constexpr int kMaxCells = 4 * kMaxK;    // bilinear: four corners per tap
-constexpr size_t kTileBudget = 64 * 1024;  // staged tiles per workgroup (two workgroups per CU)
+// Staged tiles per workgroup.  Gathers: up to 78 KB, the largest that keeps
+// two workgroups per CU (LDS is granted in 1 KB steps out of slightly less
+// than 160 KB): taller bands re-stage fewer margin rows.  The NCHW weight
+// gradient and fused backward keep 64 KB: their per-cell sums hold more
+// registers, and the smaller tiles keep more of them resident (measured
+// faster; NHWC, whose bands are shorter, gains from the taller bands).
+constexpr size_t kTileBudget = 78 * 1024;
+constexpr size_t kTileBudgetSums = 64 * 1024;
 constexpr int kXcds = 8;                // blocks are dealt round-robin to the eight XCDs
 
 enum Op { kFwd = 0, kDgrad = 1, kWgrad = 2, kBwd = 3 };
@@ -87,6 +94,7 @@ inline Plan plan_gen(int op, int layout, int N, int C, int H, int W, int K, int 
   } else {
     p.OH = p.P; p.OW = p.Q; p.SH = H; p.SW = W; p.sig = str; p.dil = 1;
   }
+  const size_t budget = layout == kNCHW && (op == kWgrad || op == kBwd) ? kTileBudgetSums : kTileBudget;
   p.ncap = (K * (mode == 1 ? 4 : 1) + 7) & ~7;  // whole groups of eight cells
   p.KB = p.ncap <= 32 ? 32 : (p.ncap <= 64 ? 64 : 128);
   // outputs per lane: four for short planes, and where the weight gradients
@@ -114,11 +122,11 @@ inline Plan plan_gen(int op, int layout, int N, int C, int H, int W, int K, int 
   for (;; p.CB /= 2) {
     // columns: the whole output width while a band of RP rows fits
     p.BQ = p.OW;
-    while (p.BQ > 8 && bytes_of(p.RP, p.BQ) > kTileBudget) p.BQ = cdiv(p.BQ, 2);
+    while (p.BQ > 8 && bytes_of(p.RP, p.BQ) > budget) p.BQ = cdiv(p.BQ, 2);
     // rows: as many as fit, in row groups of RP
     p.BP = cdiv(p.OH, p.RP) * p.RP;
-    while (p.BP > p.RP && bytes_of(p.BP, p.BQ) > kTileBudget) p.BP -= p.RP;
-    if (bytes_of(p.BP, p.BQ) <= kTileBudget || p.CB == 1) break;
+    while (p.BP > p.RP && bytes_of(p.BP, p.BQ) > budget) p.BP -= p.RP;
+    if (bytes_of(p.BP, p.BQ) <= budget || p.CB == 1) break;
   }
   if (bytes_of(p.BP, p.BQ) > kMaxLdsBytes / 2) return pl;
   p.lcb = 0;
@@ -136,7 +144,7 @@ inline Plan plan_gen(int op, int layout, int N, int C, int H, int W, int K, int 
   if (tasks < kThreads) p.G = kThreads / tasks;
   if (p.G > N) p.G = N;
   const size_t per_img = ((size_t)p.TW + (size_t)band_tiles * p.OS) * 4 * p.CB;
-  while (p.G > 1 && (size_t)p.G * per_img > kTileBudget) --p.G;
+  while (p.G > 1 && (size_t)p.G * per_img > budget) --p.G;
   p.ncb = cdiv(C, p.CB);
   // LDS: cell tables (offset and weight, tap, coefficient per cell and
   // channel, the cell count per channel), tiles, band tiles, the
