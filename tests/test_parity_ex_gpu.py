@@ -171,7 +171,17 @@ EX_MANY_TAPS = [
 ]
 
 
-@pytest.mark.parametrize("case", EX + PLANE_EX + EX_MANY_TAPS, ids=lambda c: "-".join(map(str, c)))
+# the plane shapes of the bench line's general-kernel configurations (NHWC
+# at 56 x 56, stride 2 at 224 x 224, bilinear at 56 x 56), with few images
+# and channels: the band plans depend on the plane, K and the channel block
+EX_BENCH_SHAPES = [
+    (2, 8, 56, 56, 31, "f32", "discrete8", 1, "nhwc", "floor"),
+    (1, 4, 224, 224, 31, "f32", "discrete8", 2, "nchw", "floor"),
+    (2, 3, 56, 56, 31, "f32", "discrete8", 1, "nchw", "bilinear"),
+]
+
+
+@pytest.mark.parametrize("case", EX + PLANE_EX + EX_MANY_TAPS + EX_BENCH_SHAPES, ids=lambda c: "-".join(map(str, c)))
 def test_stride_layout_sampling(case):
     N, C, H, W, K, dtype, theta, s, layout, sampling = case
     run_ex(N, C, H, W, K, dtype, theta, s, layout, sampling, label=str(case))
