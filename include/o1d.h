@@ -205,7 +205,7 @@ size_t o1d_dsc_bwd_workspace_bytes(int N, int C, int Cout, int H, int W, int K, 
 /* ---- Planning introspection (host only, no device work; for tests and tools).
  *
  * o1d_kernel_name: the kernel(s) a call with these arguments would launch,
- * e.g. "strip_gather/f32/S87/KB32" or "gen_wgrad/bf16/nhwc/RP4"; two names
+ * e.g. "strip_gather/f32/S77/KB32" or "gen_wgrad/bf16/nhwc/RP8/KB32"; two names
  * joined by '+' where o1d_bwd runs the input and weight gradients in turn.
  * op: 0 = o1d_fwd(_ex), 1 = o1d_bwd_input(_ex), 2 = o1d_bwd_weight(_ex),
  * 3 = o1d_bwd (stride 1, NCHW, O1D_FLOOR only).  `aligned` != 0 states that
