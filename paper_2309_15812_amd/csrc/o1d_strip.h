@@ -77,11 +77,19 @@ inline int fit_npw(int N, int C, int G, long long slots) {
 // whole wave (else half-wave) where that costs no plane per group, so that
 // the lanes of one wave read one band's consecutive columns (two bands in a
 // wave map their columns onto overlapping LDS banks).
+// A dense diagonal layout whose bands come in fours and whose bands hold
+// more than 8 column groups is split instead: the first 8 q column groups
+// (q = ncg / 8) of every plane of the group in half-wave blocks as above,
+// plane after plane, then the remaining column groups of all the planes,
+// band after band.  A band of 9 or more groups 4 columns apart spans more
+// than 32 banks, so band after band its first and ninth lanes would share a
+// bank in every read; split, every half-wave of blocks is conflict-free.
 struct Shape {
   int R, NC, nb, nj, jlo, ncg, ppt;
   int bq, bb;  // diagonal: half-wave blocks along the column groups and along the bands
   int dense;   // tasks one per lane, band after band
   int lpb;     // band-after-band layouts: lanes per band
+  int split;   // dense diagonal layout split into blocks and a remainder
 };
 
 __host__ __device__ inline Shape shape_of(int Hs, int Ws, int s) {
@@ -108,6 +116,7 @@ __host__ __device__ inline Shape shape_of(int Hs, int Ws, int s) {
     }
   }
   t.ppt = t.dense ? t.nb * t.lpb : blocked;
+  t.split = s && t.dense && t.nb % 4 == 0 && t.ncg > 8 && t.lpb == t.ncg;
   return t;
 }
 

@@ -581,7 +581,22 @@ __device__ __forceinline__ Block block_of(const Params& P, const Chan& ch, const
   int g = t / sh.ppt;
   const int r = t - g * sh.ppt;
   int band, cg;
-  if (SD == 0 || sh.dense) {
+  if (SD != 0 && sh.split) {
+    // blocks: 32 q (nb / 4) lanes per plane; remainder: nb rem lanes per plane
+    const int q = sh.ncg >> 3, rem = sh.ncg - 8 * q, nbk = 32 * q * (sh.nb >> 2);
+    if (t < nbk * P.G) {
+      g = t / nbk;
+      const int u = t - g * nbk, blk = u >> 5;
+      cg = 8 * (blk % q) + (u & 7);
+      band = 4 * (blk / q) + ((u >> 3) & 3);
+    } else {
+      const int v = t - nbk * P.G, rl = sh.nb * rem;
+      g = v / rl;
+      const int u = v - g * rl;
+      band = u / rem;
+      cg = 8 * q + (u - band * rem);
+    }
+  } else if (SD == 0 || sh.dense) {
     band = r / sh.lpb;
     cg = r - band * sh.lpb;
   } else {

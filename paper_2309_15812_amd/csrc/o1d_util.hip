@@ -15,14 +15,14 @@ __global__ __launch_bounds__(kThreads) void fill_zero(T* __restrict__ dst, size_
 }
 
 // dw[i] = sum over j < parts of partial[j CK + i], added in the order of j.
-// The loads are issued eight at a time ahead of their additions, so that a
-// thread waits for memory once per eight rows instead of once per row.
+// The loads are issued sixteen at a time ahead of their additions, so that a
+// thread waits for memory once per sixteen rows instead of once per row.
 template <typename T>
 __global__ __launch_bounds__(kThreads) void partial_sum(const float* __restrict__ partial, T* __restrict__ dw, int CK,
                                                         int parts) {
   const int i = blockIdx.x * blockDim.x + threadIdx.x;
   if (i >= CK) return;
-  constexpr int kBatch = 8;
+  constexpr int kBatch = 16;
   float s = 0.f;
   for (int j0 = 0; j0 < parts; j0 += kBatch) {
     float v[kBatch];

@@ -145,7 +145,8 @@ def test_edges(case, dtype):
 # Shapes the strip kernels take (W % 4 == 0, aligned tensors): non-square
 # planes in both staging frames, bands that do not fill the last strip,
 # groups of several planes with a partial last group, walks of up to 64
-# cells, and the line-kernel fallback next to them.
+# cells, the split diagonal lane layout (bands in fours of more than 8
+# column groups), and the line-kernel fallback next to them.
 EDGE_STRIP = [
     # (N, C, H, W, K, theta mode)
     (3, 5, 20, 44, 31, "uniform"),     # H != W, ragged bands, several planes per group
@@ -158,6 +159,8 @@ EDGE_STRIP = [
     (2, 3, 8, 100, 7, "uniform"),      # short and wide
     (1, 2, 64, 64, 31, "uniform"),     # more tasks than a workgroup: line kernels
     (9, 4, 28, 28, 31, "groups:8"),    # the paper's D equal groups
+    (4, 3, 24, 32, 31, "uniform"),     # split diagonal layout: 4 bands of 10 column groups
+    (2, 3, 79, 28, 15, "uniform"),     # split diagonal layout: 12 bands of 9 column groups
 ]
 
 
