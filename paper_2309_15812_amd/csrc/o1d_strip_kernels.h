@@ -307,23 +307,18 @@ struct GatherWalk<R, NC, ST, KB, KB> {
 };
 
 // One cell of the weight-gradient walk: the same window step, then the
-// cell's dot product of the lane's dy block with the window (two partial
-// sums) added to the cell's accumulator.
+// cell's dot product of the lane's dy block with the window, accumulated
+// straight into the cell's sum.
 template <int R, int NC, int ST, int C, int KB>
 __device__ __forceinline__ void wgrad_cell(float (&sl)[R + 1][NC], uint32_t& base, uint32_t lb, uint32_t vrb,
                                            uint32_t bits, const float (&dv)[R][NC], float (&acc)[KB]) {
   window_step<R, NC, ST, C, KB>(sl, base, lb, vrb, bits);
-  float t0 = 0.f, t1 = 0.f;
+  float t = acc[C];
 #pragma unroll
   for (int i = 0; i < R; ++i)
 #pragma unroll
-    for (int k = 0; k < NC; ++k) {
-      if (((i * NC + k) & 1) == 0)
-        t0 = fmaf(dv[i][k], sl[(C + i) % (R + 1)][k], t0);
-      else
-        t1 = fmaf(dv[i][k], sl[(C + i) % (R + 1)][k], t1);
-    }
-  acc[C] += t0 + t1;
+    for (int k = 0; k < NC; ++k) t = fmaf(dv[i][k], sl[(C + i) % (R + 1)][k], t);
+  acc[C] = t;
 }
 
 // acc[c] += sum over the block of dy * x[cell c + output]: the walk of one
@@ -349,7 +344,9 @@ struct WgradWalk<R, NC, ST, KB, KB> {
 // One cell of the fused backward walk over dy with the mirrored program:
 // the window step, then every window value feeds the lane's input-gradient
 // block (times the cell's weight) and the cell's weight-gradient dot
-// product (times the lane's x).  KW bounds the walk (its last cell reads
+// product (times the lane's x), which accumulates straight into the cell's
+// sum: its chain of dependent multiply-adds interleaves with the
+// independent input-gradient ones.  KW bounds the walk (its last cell reads
 // no next row); acc holds KB >= KW cells.
 template <int R, int NC, int ST, int C, int KW, int KB>
 __device__ __forceinline__ void bwd_cell(float (&sl)[R + 1][NC], uint32_t& base, uint32_t lb, uint32_t vrb,
@@ -357,19 +354,16 @@ __device__ __forceinline__ void bwd_cell(float (&sl)[R + 1][NC], uint32_t& base,
                                          float (&acc)[KB]) {
   window_step<R, NC, ST, C, KW>(sl, base, lb, vrb, bits);
   const float wc = __int_as_float(__builtin_amdgcn_readlane((int)vw, C));
-  float t0 = 0.f, t1 = 0.f;
+  float t = acc[C];
 #pragma unroll
   for (int i = 0; i < R; ++i)
 #pragma unroll
     for (int k = 0; k < NC; ++k) {
       const float v = sl[(C + i) % (R + 1)][k];
       out[i][k] = fmaf(wc, v, out[i][k]);
-      if (((i * NC + k) & 1) == 0)
-        t0 = fmaf(xv[i][k], v, t0);
-      else
-        t1 = fmaf(xv[i][k], v, t1);
+      t = fmaf(xv[i][k], v, t);
     }
-  acc[C] += t0 + t1;
+  acc[C] = t;
 }
 
 template <int R, int NC, int ST, int C, int KW, int KB>
